@@ -1,0 +1,221 @@
+/*
+ * dpool.h - C ABI of libdpool: MI355X (gfx950) paged decode attention for
+ * dual-pool token-budget serving, plus the host-side pool sizing and router
+ * that decide which pool (and so which decode shape) a request lands in.
+ *
+ * Paper: "Dual-Pool Token-Budget Routing for Cost-Efficient and Reliable LLM
+ * Serving".  Citations below name its sections, equations and algorithm.
+ *
+ * Conventions (every entry point):
+ *   - returns int status: DP_OK (0) or a negative errno-style code:
+ *       DP_EINVAL  (-22) bad argument or shape
+ *       DP_ENOMEM  (-12) block pool exhausted / workspace too small
+ *       DP_ENOTSUP (-95) head_dim, block size, dtype or GQA group not supported
+ *       DP_EIO     (-5)  a HIP runtime error (text via dp_last_error())
+ *   - no exception, abort or exit crosses the ABI; on error, caller-visible
+ *     state is left unchanged;
+ *   - the caller owns every buffer it passes.  The library owns only the
+ *     opaque dp_kv_pool handle (host memory);
+ *   - device pointers are HIP device addresses on the current device; the
+ *     decode call is asynchronous on the given stream and never synchronises.
+ */
+#ifndef DPOOL_H
+#define DPOOL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DP_OK 0
+#define DP_EIO (-5)
+#define DP_ENOMEM (-12)
+#define DP_EINVAL (-22)
+#define DP_ENOTSUP (-95)
+
+/* Text of the last error raised on the calling thread ("" if none). */
+const char* dp_last_error(void);
+
+/* Library version string. */
+const char* dp_version(void);
+
+/* ------------------------------------------------------------------------ */
+/* KV-cache sizing and paged block pool (host only).                         */
+/*                                                                           */
+/* Sec. 1.1 Eq. 1: M_seq = 2 * n_layers * n_kv_heads * head_dim             */
+/*                         * dtype_bytes * c_max   (bytes per sequence)      */
+/* Sec. 1.1 Eq. 2: N_seq = floor((m_gpu_bytes * util - m_model_bytes)       */
+/*                               / M_seq), clamped at 0                      */
+/* The pool backs N_seq sequences of ceil(c_max / block_size) blocks each   */
+/* (16-token PagedAttention blocks, pages handed out on demand: Sec. 3,     */
+/* effects 1 and 3).  Free block ids are kept in a list shuffled once with  */
+/* a seeded SplitMix64 stream (Steele, Lea & Flood 2014), so that a         */
+/* sequence's blocks are scattered over the pool as in a long-running       */
+/* server.                                                                   */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t n_layers;     /* n_l: layers whose KV this GPU holds             */
+  int32_t n_kv_heads;   /* n_h: KV heads on this GPU                        */
+  int32_t head_dim;     /* d_h                                              */
+  int32_t dtype_bytes;  /* b_dtype: 2 for bf16, 1 for fp8                   */
+  int32_t block_size;   /* tokens per block (16)                            */
+  int32_t reserved;     /* must be 0                                        */
+  int64_t c_max;        /* C_max: tokens reserved per sequence              */
+  double m_gpu_bytes;   /* M_gpu                                             */
+  double util;          /* u, fraction of HBM usable (0, 1]                  */
+  double m_model_bytes; /* M_model (weights + activations)                   */
+} dp_pool_config;
+
+typedef struct dp_kv_pool dp_kv_pool; /* opaque, host memory, owned by the library */
+
+/* Size a pool (Eq. 1, Eq. 2) and build its shuffled free list.
+ * DP_EINVAL on non-positive sizes, util outside (0,1] or reserved != 0;
+ * DP_ENOMEM if the free list cannot be allocated.  *out is set only on success. */
+int kv_pool_create(const dp_pool_config* cfg, uint64_t shuffle_seed, dp_kv_pool** out);
+
+/* Sizing results: Eq. 1 M_seq, Eq. 2 N_seq, ceil(c_max/bs), N_seq*blocks_per_seq,
+ * and the number of blocks currently free.  Any output pointer may be NULL. */
+int kv_pool_info(const dp_kv_pool* pool, int64_t* m_seq_bytes, int64_t* n_seq,
+                 int64_t* blocks_per_seq, int64_t* num_blocks, int64_t* free_blocks);
+
+/* Hand out ceil(n_tokens / block_size) blocks for one sequence (on-demand
+ * pages, Sec. 3 effect 1).  block_ids_out must hold that many int32.
+ * DP_EINVAL if n_tokens < 0 or n_tokens > c_max; DP_ENOMEM if the pool has
+ * too few free blocks (the OOM of Sec. 1.3), in which case nothing is taken. */
+int kv_pool_alloc_seq(dp_kv_pool* pool, int64_t n_tokens, int32_t* block_ids_out);
+
+/* Return blocks to the pool.  DP_EINVAL (nothing returned) if any id is out
+ * of range or already free. */
+int kv_pool_free_seq(dp_kv_pool* pool, const int32_t* block_ids, int64_t n_blocks);
+
+void kv_pool_destroy(dp_kv_pool* pool);
+
+/* ------------------------------------------------------------------------ */
+/* Token-budget routing (host only): Sec. 2.1 Eq. 3-5, Sec. 2.2 Algorithm 1 */
+/*                                                                           */
+/* Route:  c* = c_hat_k - gamma * sigma_k (Eq. 5), clamped below at c_min;   */
+/*         L_total = ceil(bytes / c*) + max_output_tokens (Eq. 3);           */
+/*         step 1  L_total > C_max(short)           -> long                  */
+/*         step 2  L_total <= b_short ? short : long                         */
+/*         step 3  spill to the other pool if the chosen one is overloaded   */
+/*                 (in_flight >= spill_theta * capacity) and the other can   */
+/*                 take the request (L_total <= its C_max, not overloaded);  */
+/*         final   L_total > C_max(chosen)          -> long.                 */
+/*         The chosen pool's in_flight is incremented.                       */
+/* OnResponse: c_obs = bytes / prompt_tokens;                                */
+/*         c_hat = beta*c_hat + (1-beta)*c_obs (Eq. 4);                      */
+/*         sigma = beta*sigma + (1-beta)*|c_obs - c_hat| (updated c_hat).    */
+/* All arithmetic is IEEE double in exactly that order (no FMA contraction), */
+/* so results are reproducible bit for bit by any IEEE-754 implementation.   */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+  double b_short;     /* B_short threshold in tokens (default 8192)        */
+  double beta;        /* EMA decay (0.95)                                   */
+  double gamma;       /* conservativeness (1.0)                             */
+  double c0;          /* cold-start bytes/token (4.0)                       */
+  double c_min;       /* floor of the conservative ratio (1.0)              */
+  double spill_theta; /* overload fraction of capacity (1.0)                */
+} dp_route_params;
+
+typedef struct {
+  double c_hat; /* calibrated bytes per token of the category */
+  double sigma; /* EMA of |c_obs - c_hat|                      */
+} dp_cat_state;
+
+typedef struct {
+  int64_t c_max;     /* longest total budget the pool can serve */
+  int64_t capacity;  /* concurrent sequences (N_seq * instances) */
+  int64_t in_flight; /* requests currently assigned             */
+} dp_pool_state;      /* pools[0] = short pool, pools[1] = long pool */
+
+/* Fill params with the paper's defaults. */
+int route_default_params(dp_route_params* params);
+
+/* Cold-start every category: c_hat = c0, sigma = 0. */
+int route_init(const dp_route_params* params, dp_cat_state* cats, int32_t n_cats);
+
+/* Route n requests in order (Algorithm 1, Route).  req_bytes[i] >= 0,
+ * 0 <= req_cat[i] < n_cats, req_max_out[i] >= 0; otherwise DP_EINVAL and
+ * nothing is written.  out_pool[i] = 0 (short) or 1 (long); out_l_total[i]
+ * = the estimated budget (either output may be NULL).  pools[*].in_flight is
+ * updated.  Host arrays, O(n), no allocation. */
+int route_requests(const dp_route_params* params, const dp_cat_state* cats, int32_t n_cats,
+                   dp_pool_state pools[2], const int64_t* req_bytes, const int32_t* req_cat,
+                   const int64_t* req_max_out, int64_t n, int8_t* out_pool,
+                   int64_t* out_l_total);
+
+/* Algorithm 1, OnResponse.  DP_EINVAL (state unchanged) if cat is out of
+ * range, req_bytes < 0 or prompt_tokens <= 0. */
+int route_on_response(const dp_route_params* params, dp_cat_state* cats, int32_t n_cats,
+                      int32_t cat, int64_t req_bytes, int64_t prompt_tokens);
+
+/* ------------------------------------------------------------------------ */
+/* Paged decode attention (device, asynchronous).                           */
+/*                                                                           */
+/* The per-step KV read the paper's cost model calls memory-bandwidth bound */
+/* (Sec. 3 effect 4; Sec. 4.4 "Why TPOT also improves"), over 16-token      */
+/* PagedAttention blocks (Sec. 3 effect 3).  For sequence s with            */
+/* T = context_lens[s] and query head h (KV head g = h / G, G = Hq / Hkv):  */
+/*   K_t = k_scale[g] * k_blocks[block_tables[s][t/16], g, t%16, :]          */
+/*   V_t = v_scale[g] * v_blocks[block_tables[s][t/16], g, t%16, :]          */
+/*   out[s,h,:] = softmax_t(scale * q[s,h,:] . K_t) @ V                     */
+/* T = 0 gives a zero row.                                                   */
+/*                                                                           */
+/* Layouts (row-major, device memory, 16-byte aligned):                      */
+/*   q            [batch, n_q_heads, head_dim]            bf16               */
+/*   k_blocks,    [num_blocks, n_kv_heads, block_size, head_dim]             */
+/*   v_blocks       bf16 (DP_KV_BF16) or OCP e4m3 bytes (DP_KV_FP8_E4M3)     */
+/*   block_tables [batch, max_blocks_per_seq] int32; entries past            */
+/*                ceil(T/16) are never read (may hold -1)                    */
+/*   context_lens [batch] int32, each <= max_context_len (a caller promise;  */
+/*                larger values are clamped, never read out of bounds)      */
+/*   k_scale,     [n_kv_heads] fp32 per-head dequantisation scales (fp8      */
+/*   v_scale        only; must be NULL for bf16)                             */
+/*   out          [batch, n_q_heads, head_dim] bf16 (DP_OUT_BF16) or fp32    */
+/*   workspace    >= paged_decode_workspace_size(shape) bytes, 256-byte      */
+/*                aligned, caller-owned; may be NULL if that size is 0       */
+/* Supported: head_dim 128, block_size 16, 1 <= Hq/Hkv <= 16.                */
+/* ------------------------------------------------------------------------ */
+#define DP_KV_BF16 0
+#define DP_KV_FP8_E4M3 1
+#define DP_OUT_BF16 0
+#define DP_OUT_FP32 1
+
+typedef struct {
+  int32_t batch;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t block_size;
+  int32_t max_blocks_per_seq;
+  int32_t max_context_len;
+  int32_t kv_dtype;         /* DP_KV_*                                        */
+  int32_t out_dtype;        /* DP_OUT_*                                       */
+  int32_t partition_tokens; /* split-K partition length; 0 = library's choice  */
+  int64_t num_blocks;       /* blocks in k_blocks / v_blocks                   */
+} dp_decode_shape;
+
+/* Bytes of workspace paged_decode_attention needs for this shape (0 when no
+ * sequence can span more than one partition).  Returns 0 for invalid shapes. */
+size_t paged_decode_workspace_size(const dp_decode_shape* shape);
+
+/* The partition length (tokens) the library uses for this shape. */
+int32_t paged_decode_partition_tokens(const dp_decode_shape* shape);
+
+/* Launch the decode attention on `stream` (a hipStream_t; NULL = default
+ * stream).  Validates the shape and pointer alignment on the host
+ * (DP_EINVAL / DP_ENOTSUP / DP_ENOMEM for a short workspace), then enqueues
+ * one partition kernel and, when some sequence spans several partitions, one
+ * log-sum-exp merge kernel.  DP_EIO if a launch fails. */
+int paged_decode_attention(const void* q, const void* k_blocks, const void* v_blocks,
+                           const int32_t* block_tables, const int32_t* context_lens,
+                           float scale, const float* k_scale, const float* v_scale,
+                           void* out, const dp_decode_shape* shape, void* workspace,
+                           size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DPOOL_H */

@@ -1,0 +1,128 @@
+"""Token-budget routing: Eq. 3-5 and Algorithm 1 (Sec. 2.1-2.2), in IEEE float64.
+
+Test infrastructure only (see the package header).
+
+Steps, in the paper's order:
+
+Route(r, k)                                               (Algorithm 1, Route)
+  c*      = c_hat_k - gamma * sigma_k                      (Eq. 5, conservative ratio)
+  L_total = ceil(|r| / c*) + max_output_tokens             (Eq. 3, total token budget)
+  step 1  feasibility: L_total > C_max(short)  -> long     (strict >)
+  step 2  budget:      L_total <= B_short      -> short, else long  (inclusive <=)
+  step 3  spillover:   preferred pool overloaded and the alternate can serve r
+                       -> alternate
+  final   safety:      L_total > C_max(chosen) -> long
+OnResponse(r, k, prompt_tokens)                           (Algorithm 1, OnResponse)
+  c_obs   = |r| / prompt_tokens                            (Eq. 4)
+  c_hat_k = beta * c_hat_k + (1 - beta) * c_obs            (Eq. 4 EMA, beta = 0.95)
+  sigma_k = EMA(sigma_k, |c_obs - c_hat_k|), same beta, using the c_hat_k just updated
+
+Defaults: c0 = 4.0 (cold start), beta = 0.95, gamma = 1.0, B_short = 8192.
+
+Readings where the paper is silent (each also listed in the design doc):
+  * sigma starts at 0 (its initial value is not given).
+  * c* is clamped below at c_min = 1.0 byte/token, so that gamma * sigma >= c_hat
+    cannot give a zero or negative ratio.
+  * "overloaded" is in_flight >= spill_theta * capacity (the paper names queue
+    depth or utilization, without a formula); "the alternate pool can serve r"
+    is L_total <= C_max(alternate) and the alternate not overloaded.
+  * Each routed request increments the chosen pool's in_flight, so a batch is
+    routed sequentially.
+  * The feasibility branch returns straight away (no spillover), as the
+    algorithm's early return says.
+  * (1 - beta) is evaluated at run time (0.050000000000000044 for 0.95).
+  * OnResponse with prompt_tokens <= 0 is rejected and changes nothing.
+
+Parity: pinned by hand-computed boundary vectors at cold start (8192 -> short,
+8193 -> long), by the closed form of n identical observations
+(c_hat_n = c + beta^n (c0 - c), sigma_n = n (1 - beta) beta^n |c0 - c|), and by
+the safety invariant (the chosen pool always has C_max >= L_total).
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+
+SHORT = 0
+LONG = 1
+
+
+@dataclass
+class RouteParams:
+    b_short: float = 8192.0
+    beta: float = 0.95
+    gamma: float = 1.0
+    c0: float = 4.0
+    c_min: float = 1.0
+    spill_theta: float = 1.0
+
+
+@dataclass
+class CatState:
+    c_hat: float
+    sigma: float
+
+
+@dataclass
+class PoolState:
+    c_max: int
+    capacity: int
+    in_flight: int = 0
+
+
+def init_categories(params: RouteParams, n_cats: int):
+    return [CatState(params.c0, 0.0) for _ in range(n_cats)]
+
+
+def conservative_ratio(params: RouteParams, cat: CatState) -> float:
+    c = cat.c_hat - params.gamma * cat.sigma
+    if c < params.c_min:
+        c = params.c_min
+    return c
+
+
+def token_budget(req_bytes: int, max_out: int, c_star: float) -> int:
+    return int(math.ceil(float(req_bytes) / c_star)) + int(max_out)
+
+
+def overloaded(params: RouteParams, pool: PoolState) -> bool:
+    return float(pool.in_flight) >= params.spill_theta * float(pool.capacity)
+
+
+def route_one(params: RouteParams, cats, pools, req_bytes: int, cat: int, max_out: int):
+    """Algorithm 1 Route for one request; updates pools[chosen].in_flight. Returns (pool, L_total)."""
+    c_star = conservative_ratio(params, cats[cat])
+    l_total = token_budget(req_bytes, max_out, c_star)
+    if l_total > pools[SHORT].c_max:          # step 1: feasibility
+        choice = LONG
+    else:
+        choice = SHORT if l_total <= params.b_short else LONG   # step 2
+        alt = 1 - choice                                          # step 3
+        if (overloaded(params, pools[choice]) and l_total <= pools[alt].c_max
+                and not overloaded(params, pools[alt])):
+            choice = alt
+        if l_total > pools[choice].c_max:     # final safety check
+            choice = LONG
+    pools[choice].in_flight += 1
+    return choice, l_total
+
+
+def route_requests(params: RouteParams, cats, pools, req_bytes, req_cat, req_max_out):
+    out_pool, out_l = [], []
+    for b, k, mo in zip(req_bytes, req_cat, req_max_out):
+        p, l_total = route_one(params, cats, pools, int(b), int(k), int(mo))
+        out_pool.append(p)
+        out_l.append(l_total)
+    return out_pool, out_l
+
+
+def on_response(params: RouteParams, cats, cat: int, req_bytes: int, prompt_tokens: int) -> bool:
+    """Algorithm 1 OnResponse.  Returns False (state unchanged) when prompt_tokens <= 0."""
+    if prompt_tokens <= 0:
+        return False
+    st = cats[cat]
+    c_obs = float(req_bytes) / float(prompt_tokens)
+    one_minus_beta = 1.0 - params.beta
+    st.c_hat = params.beta * st.c_hat + one_minus_beta * c_obs
+    st.sigma = params.beta * st.sigma + one_minus_beta * abs(c_obs - st.c_hat)
+    return True
