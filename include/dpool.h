@@ -193,7 +193,10 @@ typedef struct {
   int32_t max_context_len;
   int32_t kv_dtype;         /* DP_KV_*                                        */
   int32_t out_dtype;        /* DP_OUT_*                                       */
-  int32_t partition_tokens; /* split-K partition length; 0 = library's choice  */
+  int32_t partition_tokens; /* split-K partition length in tokens, a multiple  */
+                            /* of 16 (bf16) or 32 (fp8); 0 = library's choice */
+  int32_t pipeline_stages;  /* KV tiles in flight per wave, 2..4; 0 = choice  */
+  int32_t reserved;         /* must be 0                                      */
   int64_t num_blocks;       /* blocks in k_blocks / v_blocks                   */
 } dp_decode_shape;
 
@@ -207,13 +210,37 @@ int32_t paged_decode_partition_tokens(const dp_decode_shape* shape);
 /* Launch the decode attention on `stream` (a hipStream_t; NULL = default
  * stream).  Validates the shape and pointer alignment on the host
  * (DP_EINVAL / DP_ENOTSUP / DP_ENOMEM for a short workspace), then enqueues
- * one partition kernel and, when some sequence spans several partitions, one
- * log-sum-exp merge kernel.  DP_EIO if a launch fails. */
+ * the partition phase and, when some sequence spans several partitions, the
+ * merge phase (the two calls below, in that order).  DP_EIO if a launch
+ * fails. */
 int paged_decode_attention(const void* q, const void* k_blocks, const void* v_blocks,
                            const int32_t* block_tables, const int32_t* context_lens,
                            float scale, const float* k_scale, const float* v_scale,
                            void* out, const dp_decode_shape* shape, void* workspace,
                            size_t workspace_bytes, void* stream);
+
+/* Phase 1 alone (same arguments and checks as paged_decode_attention).
+ * Splits every sequence into partitions of paged_decode_partition_tokens()
+ * tokens (split-K over the context).  Rows of sequences that fit in one
+ * partition are written to `out` directly; every other (sequence, head,
+ * partition) leaves its softmax partial in the workspace:
+ *   o_p [batch, n_q_heads, max_parts, 128] fp32, normalised by l_p,
+ *   (m_p, l_p) [batch, n_q_heads, max_parts, 2] fp32, m_p in log2 units,
+ * with max_parts = ceil(max_context_len / partition_tokens), o_p at offset 0
+ * and (m_p, l_p) at the next 256-byte boundary.  A context-parallel caller
+ * can exchange these partials between devices before phase 2. */
+int paged_decode_partition(const void* q, const void* k_blocks, const void* v_blocks,
+                           const int32_t* block_tables, const int32_t* context_lens,
+                           float scale, const float* k_scale, const float* v_scale,
+                           void* out, const dp_decode_shape* shape, void* workspace,
+                           size_t workspace_bytes, void* stream);
+
+/* Phase 2 alone: for every sequence that spans several partitions, merge its
+ * partials with log-sum-exp weights, M = max_p m_p,
+ * w_p = l_p * 2^(m_p - M), out = sum_p w_p o_p / sum_p w_p, and write `out`.
+ * A no-op (DP_OK) when no sequence can span two partitions. */
+int paged_decode_merge(const int32_t* context_lens, void* out, const dp_decode_shape* shape,
+                       void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -1,0 +1,93 @@
+// Token-budget pool routing: Sec. 2.1 Eq. 3-5 and Sec. 2.2 Algorithm 1.
+// Host only.  Compiled with -ffp-contract=off: every double operation is
+// rounded on its own, in the order written, so that any IEEE-754 double
+// implementation of the same steps agrees bit for bit.
+#include <cmath>
+#include <cstdint>
+
+#include "common.h"
+
+namespace {
+
+constexpr int kShort = 0;
+constexpr int kLong = 1;
+
+bool overloaded(const dp_route_params* p, const dp_pool_state& pool) {
+  return (double)pool.in_flight >= p->spill_theta * (double)pool.capacity;
+}
+
+// Eq. 5: conservative bytes-per-token ratio, floored at c_min.
+double conservative_ratio(const dp_route_params* p, const dp_cat_state& c) {
+  double r = c.c_hat - p->gamma * c.sigma;
+  if (r < p->c_min) r = p->c_min;
+  return r;
+}
+
+}  // namespace
+
+extern "C" int route_default_params(dp_route_params* params) {
+  if (!params) return dpool::fail(DP_EINVAL, "route_default_params: null");
+  params->b_short = 8192.0;  // Sec. 2.2 "Choosing B_short"
+  params->beta = 0.95;       // Eq. 4
+  params->gamma = 1.0;       // Eq. 5
+  params->c0 = 4.0;          // Sec. 2.1 cold start
+  params->c_min = 1.0;
+  params->spill_theta = 1.0;
+  return DP_OK;
+}
+
+extern "C" int route_init(const dp_route_params* params, dp_cat_state* cats, int32_t n_cats) {
+  if (!params || (!cats && n_cats > 0) || n_cats < 0) return dpool::fail(DP_EINVAL, "route_init: bad arguments");
+  for (int32_t k = 0; k < n_cats; ++k) {
+    cats[k].c_hat = params->c0;
+    cats[k].sigma = 0.0;
+  }
+  return DP_OK;
+}
+
+extern "C" int route_requests(const dp_route_params* params, const dp_cat_state* cats, int32_t n_cats,
+                              dp_pool_state pools[2], const int64_t* req_bytes, const int32_t* req_cat,
+                              const int64_t* req_max_out, int64_t n, int8_t* out_pool, int64_t* out_l_total) {
+  using dpool::fail;
+  if (!params || !cats || !pools || n_cats <= 0 || n < 0) return fail(DP_EINVAL, "route_requests: bad arguments");
+  if (n == 0) return DP_OK;
+  if (!req_bytes || !req_cat || !req_max_out) return fail(DP_EINVAL, "route_requests: null request arrays");
+  if (!(params->c_min > 0.0)) return fail(DP_EINVAL, "route_requests: c_min must be > 0");
+  for (int64_t i = 0; i < n; ++i) {
+    if (req_bytes[i] < 0 || req_max_out[i] < 0 || req_cat[i] < 0 || req_cat[i] >= n_cats)
+      return fail(DP_EINVAL, "route_requests: request %lld has bytes/max_out < 0 or category out of range",
+                  (long long)i);
+  }
+  for (int64_t i = 0; i < n; ++i) {
+    const double c_star = conservative_ratio(params, cats[req_cat[i]]);          // Eq. 5
+    const int64_t l_total = (int64_t)std::ceil((double)req_bytes[i] / c_star) + req_max_out[i];  // Eq. 3
+    int choice;
+    if (l_total > pools[kShort].c_max) {  // step 1: feasibility
+      choice = kLong;
+    } else {
+      choice = ((double)l_total <= params->b_short) ? kShort : kLong;  // step 2: budget
+      const int alt = 1 - choice;                                      // step 3: spillover
+      if (overloaded(params, pools[choice]) && l_total <= pools[alt].c_max && !overloaded(params, pools[alt]))
+        choice = alt;
+      if (l_total > pools[choice].c_max) choice = kLong;  // final safety check
+    }
+    pools[choice].in_flight += 1;
+    if (out_pool) out_pool[i] = (int8_t)choice;
+    if (out_l_total) out_l_total[i] = l_total;
+  }
+  return DP_OK;
+}
+
+extern "C" int route_on_response(const dp_route_params* params, dp_cat_state* cats, int32_t n_cats, int32_t cat,
+                                 int64_t req_bytes, int64_t prompt_tokens) {
+  using dpool::fail;
+  if (!params || !cats || cat < 0 || cat >= n_cats || req_bytes < 0 || prompt_tokens <= 0)
+    return fail(DP_EINVAL, "route_on_response: bad arguments (cat %d, bytes %lld, prompt_tokens %lld)", cat,
+                (long long)req_bytes, (long long)prompt_tokens);
+  dp_cat_state& st = cats[cat];
+  const double c_obs = (double)req_bytes / (double)prompt_tokens;       // Eq. 4
+  const double one_minus_beta = 1.0 - params->beta;
+  st.c_hat = params->beta * st.c_hat + one_minus_beta * c_obs;         // Eq. 4 EMA
+  st.sigma = params->beta * st.sigma + one_minus_beta * std::fabs(c_obs - st.c_hat);  // uncertainty EMA
+  return DP_OK;
+}

@@ -21,3 +21,15 @@ def gpu_lib():
         pytest.skip("no GPU visible")
     from paper_2604_08075_amd import binding
     return binding
+
+
+@pytest.fixture(scope="session")
+def host_lib():
+    """The product binding for host-only calls (builds libdpool.so if nothing is built yet)."""
+    from paper_2604_08075_amd import binding
+    import os
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2604_08075_amd import build
+        build.build()
+    binding.lib()
+    return binding

@@ -1,0 +1,218 @@
+"""GPU parity of paged_decode_attention (through the C ABI) against the fp64 oracle.
+
+Tolerances are fixed by the target: max abs error 1.5e-2 with bf16 KV and
+3e-2 with fp8 e4m3 KV, on the bf16 output the library ships (the fp32
+output variant is checked to the same bar).  Integer-like properties
+(block permutation, poisoned unused blocks, determinism, pipeline variants)
+are checked bit for bit.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import workloads
+from oracle import attention, numerics
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"bf16": 1.5e-2, "fp8_e4m3": 3e-2}
+
+
+def note(msg):
+    print(f"[gpu-test] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def oracle_out(w, seqs=None):
+    return attention.paged_decode_attention(w.q_bits, w.k_store, w.v_store, w.block_tables, w.context_lens, w.scale,
+                                            kv_format=w.kv_format, k_scale=w.k_scale, v_scale=w.v_scale, seqs=seqs)
+
+
+def gpu_out(lib, w, dev=None, out_fp32=False, P=0, stages=0, layer=0):
+    d = dev if dev is not None else workloads.to_device(w)
+    dec = lib.PagedDecoder(w.batch, w.n_q_heads, w.n_kv_heads, w.max_blocks_per_seq, max(w.max_context_len, 0),
+                           w.num_blocks, kv_fp8=w.kv_format == "fp8_e4m3", out_fp32=out_fp32, partition_tokens=P,
+                           pipeline_stages=stages)
+    out = dec.new_out()
+    dec(d["q"], d["k"][layer], d["v"][layer], d["block_tables"], d["context_lens"], w.scale, out, d["k_scale"],
+        d["v_scale"])
+    torch.cuda.synchronize()
+    return out.float().cpu().numpy()
+
+
+def max_err(got, ref, seqs):
+    return float(np.abs(got[seqs] - ref[seqs]).max())
+
+
+def sample_seqs(w, n):
+    if w.batch <= n:
+        return list(range(w.batch))
+    ctx = w.context_lens
+    pick = {int(np.argmax(ctx)), int(np.argmin(ctx))}
+    rng = np.random.default_rng(1234)
+    for s in rng.permutation(w.batch):
+        if len(pick) >= n:
+            break
+        pick.add(int(s))
+    return sorted(pick)
+
+
+@pytest.mark.parametrize("cfg,n_sample", [(1, 4), (2, 24), (3, 5), (4, 16), (5, 24)])
+def test_config_parity(gpu_lib, cfg, n_sample):
+    note(f"config {cfg}: building workload")
+    w = workloads.make_config(cfg)
+    seqs = sample_seqs(w, n_sample)
+    note(f"config {cfg}: B={w.batch} max_ctx={w.max_context_len} sampled={len(seqs)}")
+    dev = workloads.to_device(w)
+    got = gpu_out(gpu_lib, w, dev)
+    ref = oracle_out(w, seqs)
+    err = max_err(got, ref, seqs)
+    note(f"config {cfg}: max abs err {err:.3e} (bf16 out)")
+    assert np.isfinite(got).all()
+    assert err <= TOL[w.kv_format]
+    got32 = gpu_out(gpu_lib, w, dev, out_fp32=True)
+    err32 = max_err(got32, ref, seqs)
+    note(f"config {cfg}: max abs err {err32:.3e} (fp32 out)")
+    assert err32 <= TOL[w.kv_format]
+
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
+@pytest.mark.parametrize("G", [1, 4, 8, 16])
+@pytest.mark.parametrize("P", [0, 32, 64, 512])
+def test_random_shapes_ragged(gpu_lib, kv, G, P):
+    ctx = [1, 15, 16, 17, 31, 33, 64, 100, 513, 1000, 2049]
+    Hkv = 2
+    note(f"random shapes kv={kv} G={G} P={P}")
+    w = workloads.make_workload(len(ctx), G * Hkv, Hkv, ctx, c_max=2560, kv_format=kv, seed=G * 100 + P)
+    got = gpu_out(gpu_lib, w, P=P, out_fp32=True)
+    ref = oracle_out(w)
+    err = max_err(got, ref, list(range(len(ctx))))
+    note(f"  max abs err {err:.3e}")
+    assert err <= TOL[kv]
+
+
+def test_partition_invariance(gpu_lib):
+    """Different split-K partitionings agree to the bound the arithmetic gives.
+
+    The probabilities are rounded to bf16 (relative error <= 2^-9) relative to
+    the running max, and that max depends on where partitions start.  Each
+    output row is a convex combination of V rows, so perturbing every weight by
+    a relative 2^-9 moves it by at most 2^-9 * max_t |v_t - out| (first order);
+    two partitionings differ by at most twice that (plus fp32 rounding).
+    """
+    note("partition invariance")
+    ctx = [3000, 1, 700, 4096, 2500]
+    w = workloads.make_workload(len(ctx), 32, 4, ctx, c_max=4096, seed=77)
+    dev = workloads.to_device(w)
+    ref = oracle_out(w)
+    bound = np.zeros((w.batch, w.n_q_heads, 1))
+    for s_, T in enumerate(ctx):
+        for h in range(w.n_q_heads):
+            V = np.concatenate([numerics.decode_bf16(w.v_store[np.array([b])][0, h // 8])
+                                for b in w.block_tables[s_, :-(-T // 16)]])[:T]
+            bound[s_, h] = 2 * 2.0 ** -9 * np.abs(V - ref[s_, h]).max() + 1e-6
+    outs = [gpu_out(gpu_lib, w, dev, out_fp32=True, P=P) for P in (16, 64, 256, 512, 1024, 4096)]
+    for o in outs[1:]:
+        diff = np.abs(o - outs[0])
+        note(f"  max diff {diff.max():.3e}, mean diff {diff.mean():.3e}")
+        assert (diff <= bound).all()
+
+
+def test_one_token_context_returns_v_exactly(gpu_lib):
+    note("ctx=1 returns V")
+    w = workloads.make_workload(5, 16, 2, [1] * 5, c_max=64, seed=4)
+    got = gpu_out(gpu_lib, w)
+    for s in range(5):
+        blk = w.block_tables[s, 0]
+        for h in range(16):
+            v = numerics.decode_bf16(w.v_store[np.array([blk])][0, h // 8, 0])
+            assert np.array_equal(got[s, h], v)
+
+
+def test_empty_context_gives_zero_rows(gpu_lib):
+    note("ctx=0 rows")
+    w = workloads.make_workload(4, 8, 2, [0, 40, 0, 7], c_max=64, seed=5)
+    for fp32 in (False, True):
+        got = gpu_out(gpu_lib, w, out_fp32=fp32)
+        assert np.array_equal(got[[0, 2]], np.zeros((2, 8, 128)))
+        ref = oracle_out(w, [1, 3])
+        assert max_err(got, ref, [1, 3]) <= TOL["bf16"]
+
+
+def test_block_permutation_is_bit_exact(gpu_lib):
+    note("block permutation")
+    w = workloads.make_workload(6, 64, 8, [5, 300, 1024, 17, 2000, 64], c_max=2048, seed=6, num_blocks=600)
+    base = gpu_out(gpu_lib, w)
+    rng = np.random.default_rng(0)
+    pi = rng.permutation(w.num_blocks)
+    w2 = workloads.make_workload(6, 64, 8, [5, 300, 1024, 17, 2000, 64], c_max=2048, seed=6, num_blocks=600)
+    # move each physical block b to pi[b] and fix the table up
+    for st in (w2.k_store, w2.v_store):
+        st.used_ids = pi[st.used_ids]
+        st.slot = np.full(st.num_blocks, -1, dtype=np.int64)
+        st.slot[st.used_ids] = np.arange(len(st.used_ids))
+    w2.block_tables = np.where(w.block_tables >= 0, pi[np.maximum(w.block_tables, 0)], -1).astype(np.int32)
+    moved = gpu_out(gpu_lib, w2)
+    assert np.array_equal(moved, base)
+
+
+def test_unused_blocks_never_read(gpu_lib):
+    note("poisoned vs junk unused blocks")
+    w = workloads.make_workload(4, 16, 2, [33, 700, 5, 129], c_max=1024, seed=7, num_blocks=400)
+    a = gpu_out(gpu_lib, w, workloads.to_device(w, poison_unused=True))
+    dev = workloads.to_device(w, poison_unused=True)
+    used = torch.zeros(w.num_blocks, dtype=torch.bool, device="cuda")
+    used[torch.from_numpy(w.k_store.used_ids).cuda()] = True
+    junk = torch.randint(-30000, 30000, dev["k"].shape, dtype=torch.int16, device="cuda")
+    dev["k"][:, ~used] = junk[:, ~used]
+    dev["v"][:, ~used] = junk[:, ~used]
+    b = gpu_out(gpu_lib, w, dev)
+    assert np.isfinite(a).all()
+    assert np.array_equal(a, b)
+
+
+def test_deterministic_and_stage_variants_bit_exact(gpu_lib):
+    note("determinism + pipeline stage variants")
+    for kv in ("bf16", "fp8_e4m3"):
+        w = workloads.make_workload(8, 64, 4, [1, 100, 900, 3000, 17, 4096, 256, 2222], c_max=4096, kv_format=kv,
+                                    seed=8)
+        dev = workloads.to_device(w)
+        ref = gpu_out(gpu_lib, w, dev, stages=2)
+        assert np.array_equal(gpu_out(gpu_lib, w, dev, stages=2), ref)
+        for st in (3, 4):
+            assert np.array_equal(gpu_out(gpu_lib, w, dev, stages=st), ref)
+
+
+def test_longest_context_and_gqa16_bf16(gpu_lib):
+    note("C_max 65536 sequence, GQA 16 bf16")
+    w = workloads.make_workload(2, 32, 2, [65536, 40000], c_max=65536, seed=9)
+    got = gpu_out(gpu_lib, w)
+    ref = oracle_out(w)
+    err = max_err(got, ref, [0, 1])
+    note(f"  max abs err {err:.3e}")
+    assert err <= TOL["bf16"]
+
+
+def test_rotated_layers_read_their_own_pool(gpu_lib):
+    note("layer rotation")
+    w = workloads.make_workload(3, 16, 2, [100, 200, 300], c_max=512, seed=10)
+    dev = workloads.to_device(w, layers=3)
+    outs = [gpu_out(gpu_lib, w, dev, layer=l) for l in range(3)]
+    assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])
+
+
+def test_two_phase_calls_equal_one_shot(gpu_lib):
+    note("partition + merge phases == one-shot call")
+    w = workloads.make_workload(5, 32, 4, [3000, 1, 700, 4096, 2500], c_max=4096, seed=12)
+    dev = workloads.to_device(w)
+    one = gpu_out(gpu_lib, w, dev, P=256)
+    dec = gpu_lib.PagedDecoder(w.batch, w.n_q_heads, w.n_kv_heads, w.max_blocks_per_seq, w.max_context_len,
+                               w.num_blocks, partition_tokens=256)
+    out = dec.new_out()
+    dec.partition(dev["q"], dev["k"][0], dev["v"][0], dev["block_tables"], dev["context_lens"], w.scale, out)
+    dec.merge(dev["context_lens"], out)
+    torch.cuda.synchronize()
+    assert np.array_equal(out.float().cpu().numpy(), one)

@@ -238,3 +238,34 @@ def make_config(i: int, seed: int | None = None, poison: bool = True) -> Workloa
     return make_workload(c["batch"], c["n_q_heads"], c["n_kv_heads"], ctx, c["c_max"], c["kv"],
                          num_blocks=c.get("num_blocks"), seed=seed, poison=poison, config=i,
                          name=c["name"], rng=rng)
+
+
+def to_device(w: Workload, device="cuda", layers: int = 1, poison_unused: bool = True):
+    """Place a workload in device memory (torch tensors; plumbing only).
+
+    Returns a dict with q [B, Hq, D] (bf16 codes as int16), k/v pools
+    [layers, num_blocks, Hkv, bs, D] (int16 bf16 codes or uint8 e4m3 codes;
+    every layer holds the same tiles at the same block ids), block_tables,
+    context_lens (int32) and the fp8 scales.  Unused pool blocks are NaN codes
+    when poison_unused, else left unwritten.
+    """
+    fp8 = w.kv_format == "fp8_e4m3"
+    tdt = torch.uint8 if fp8 else torch.int16
+    nan = int(E4M3_NAN) if fp8 else int(np.int16(np.uint16(BF16_NAN).view(np.int16)))
+    shape = (layers, w.num_blocks, w.n_kv_heads, w.block_size, w.head_dim)
+    ids = torch.from_numpy(w.k_store.used_ids).to(device)
+    out = {}
+    for name, store in (("k", w.k_store), ("v", w.v_store)):
+        pool = torch.full(shape, nan, dtype=tdt, device=device) if poison_unused else torch.empty(
+            shape, dtype=tdt, device=device)
+        tiles = torch.from_numpy(store.tiles.view(np.int16) if not fp8 else store.tiles).to(device)
+        for l in range(layers):
+            pool[l].index_copy_(0, ids, tiles)
+        out[name] = pool
+        del tiles
+    out["q"] = torch.from_numpy(w.q_bits.view(np.int16)).to(device)
+    out["block_tables"] = torch.from_numpy(w.block_tables).to(device)
+    out["context_lens"] = torch.from_numpy(w.context_lens).to(device)
+    out["k_scale"] = torch.from_numpy(w.k_scale).to(device) if fp8 else None
+    out["v_scale"] = torch.from_numpy(w.v_scale).to(device) if fp8 else None
+    return out
