@@ -10,35 +10,43 @@
 //     K_t / V_t = row t%16 of tile (block_tables[s][t/16], g), times the
 //     per-head fp8 scale when the cache is e4m3.
 //
-// Design (one launch of the partition kernel, plus one merge launch when a
-// sequence spans several partitions):
-//   * one workgroup per (partition, KV head, sequence); a partition is P
-//     consecutive tokens, so long contexts are split across workgroups
-//     ("split-K") and merged afterwards with log-sum-exp weights;
-//   * the workgroup's NW waves stream disjoint "units" of the partition (one
-//     16-token block for bf16, two blocks for fp8) through private LDS stages
-//     with gfx950's direct-to-LDS 128-bit loads (global_load_lds_dwordx4), so
-//     NSTAGE-1 units per wave stay in flight with no VGPR cost;
-//   * every K/V tile of a (block, KV head) is one contiguous 4 KiB (bf16) or
-//     2 KiB (fp8) region and is read exactly once; all G query heads of the
-//     GQA group use it from LDS;
-//   * S^T = K Q^T runs on MFMA (v_mfma_f32_16x16x32_bf16: 16 tokens x 16
-//     heads, query heads past G are zero padding).  Its accumulator layout is
-//     exactly the B operand of O^T = V^T P, so the probabilities never move
-//     between lanes; V^T comes straight out of LDS through the transposing
-//     reads ds_read_b64_tr_b16 / ds_read_b64_tr_b8;
-//   * the online softmax runs in base 2 (scale * log2 e folded into one
-//     multiply), with the per-head max reduced across the four 16-lane rows
-//     by cross-lane swizzles; O^T keeps each head in one lane column, so the
-//     running-max rescale is lane-local;
-//   * fp8 e4m3 tiles are widened to bf16 exactly (v_cvt_scalef32_pk_bf16_fp8
-//     with scale 1) and the per-head K scale is folded into the score
-//     multiplier, the V scale into the final normalisation.
+// Work decomposition (stream-K over the KV stream).  The cached tokens of
+// every (sequence, KV head) "segment" form one flat stream of units (a unit
+// is one 16-token block for bf16, two for fp8), segments in sequence-major,
+// head-minor order.  A persistent grid sized to the device gives every wave
+// one contiguous, equal-length slice of that stream, so the load is balanced
+// to one unit however skewed the context lengths are, and no workgroup is
+// launched without work.  A wave walks its slice across segment boundaries
+// without draining its load pipeline.  A segment that lies wholly inside one
+// slice is finished in registers and written to `out`; a segment cut by slice
+// boundaries leaves one softmax partial per piece (each wave has at most two
+// such pieces: its first and its last), merged afterwards with log-sum-exp
+// weights by the merge kernel.
+//
+// Per wave, the hot loop:
+//   * gfx950's direct-to-LDS loads (global_load_lds_dwordx4, 16 B per lane)
+//     move each unit's K and V tiles into one of NSTAGE private LDS stages,
+//     so NSTAGE-1 units stay in flight at no VGPR cost; a (block, head) tile
+//     is one contiguous 4 KiB (bf16) / 2 KiB (fp8) region read exactly once;
+//   * S^T = K Q^T on MFMA (v_mfma_f32_16x16x32_bf16: 16 tokens x 16 query
+//     heads, heads past the GQA group are zero padding), so every query head
+//     of the group reuses the tile from LDS;
+//   * the score accumulator layout is exactly the B operand of O^T = V^T P,
+//     so probabilities never move between lanes; V^T comes out of LDS
+//     through the transposing reads ds_read_b64_tr_b16 / _b8;
+//   * online softmax in base 2 (scale * log2 e folded into one multiply),
+//     the per-head max crossing the four 16-lane rows by two swizzles; O^T
+//     keeps each head in one lane column, so the running-max rescale is
+//     lane-local;
+//   * fp8 e4m3 tiles widen to bf16 exactly (v_cvt_scalef32_pk_bf16_fp8 with
+//     scale 1); the per-head K scale folds into the score multiplier, the V
+//     scale into the final normalisation.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 
 #include "common.h"
 
@@ -59,23 +67,28 @@ typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
 constexpr int kHeadDim = 128;
 constexpr int kBlock = 16;
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kWaves = 4;                 // waves per workgroup
+constexpr int kMaxUnitsPerWave = 256;     // the host sizes the grid so that no slice is longer
 
-struct DecodeArgs {
-  const uint16_t* q;          // [B, Hq, 128] bf16
-  const char* k;              // [num_blocks, Hkv, 16, 128] bf16 or e4m3
+struct StreamArgs {
+  const uint16_t* q;            // [B, Hq, 128] bf16
+  const char* k;                // [num_blocks, Hkv, 16, 128] bf16 or e4m3
   const char* v;
   const int32_t* block_tables;  // [B, max_blocks_per_seq]
   const int32_t* context_lens;  // [B]
-  const float* k_scale;       // [Hkv] (fp8)
+  const float* k_scale;         // [Hkv] (fp8)
   const float* v_scale;
-  void* out;                  // [B, Hq, 128] bf16 or fp32
-  float* part_o;              // [B, Hq, max_parts, 128]
-  float* part_ml;             // [B, Hq, max_parts, 2]  (max in log2 units, sum)
-  float qk_scale_log2;        // scale * log2(e)
+  void* out;                    // [B, Hq, 128] bf16 or fp32
+  float* rec_o;                 // [waves, 2, G, 128]  partial outputs (normalised)
+  float* rec_ml;                // [waves, 2, G, 2]    (max in log2 units, sum)
+  int32_t* plan;                // [B + 2]: unit prefix over sequences, then the slice length
+  int32_t* hdr;                 // [waves, 4]: (s, g, a0, nus) of the segment a wave terminates, nus = 0 if none
+  float qk_scale_log2;          // scale * log2(e)
   int32_t batch, hq, hkv, group;
-  int32_t max_blocks_per_seq, max_ctx, part_tokens, max_parts;
-  int32_t num_blocks_m1;      // num_blocks - 1 (block ids are clamped into range)
+  int32_t max_blocks_per_seq, max_ctx;
+  int32_t num_blocks_m1;        // num_blocks - 1 (block ids are clamped into range)
   int32_t out_fp32;
+  int32_t min_chunk;            // minimum units per slice
 };
 
 // ----- LDS swizzles: 16-byte chunk permutations per row, chosen so that the
@@ -86,19 +99,6 @@ __device__ __forceinline__ int swz_bf16(int row) {  // 16 chunks per 256-byte ro
 }
 __device__ __forceinline__ int swz_fp8(int row) {  // 8 chunks per 128-byte row
   return (row & 3) | ((((row >> 2) ^ (row >> 3)) & 1) << 2);
-}
-
-__device__ __forceinline__ void wait_vmcnt(int n) {
-  // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
-  // vmcnt[3:0] | expcnt[6:4]=7 | lgkmcnt[11:8]=15 | vmcnt[5:4] in [15:14]).
-  switch (n) {
-#define WV(N) \
-  case N: __builtin_amdgcn_s_waitcnt(((N) & 15) | (7 << 4) | (15 << 8) | (((N) >> 4) << 14)); break;
-    WV(0) WV(1) WV(2) WV(3) WV(4) WV(5) WV(6) WV(7) WV(8) WV(9) WV(10) WV(11) WV(12) WV(13) WV(14) WV(15)
-    WV(16) WV(17) WV(18) WV(19) WV(20) WV(21) WV(22) WV(23) WV(24) WV(25) WV(26) WV(27) WV(28)
-#undef WV
-    default: __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); break;
-  }
 }
 
 __device__ __forceinline__ float xor_max(float x) {
@@ -122,10 +122,11 @@ __device__ __forceinline__ bf16x8 fp8x8_to_bf16(int lo, int hi) {
   return r;
 }
 
-// Transposing LDS reads, issued as inline asm: through the builtins the
-// compiler cannot tell them apart from the in-flight direct-to-LDS loads and
-// waits for every outstanding global load first.  The caller waits for
-// completion with lds_wait_*(), which also carries the data dependency.
+// LDS reads of the stage buffers, issued as inline asm: the compiler cannot
+// tell them apart from the in-flight direct-to-LDS loads into the other
+// stages and would wait for every outstanding global load first.  The caller
+// waits for completion with lds_wait_*(), which also carries the data
+// dependency into the consumers.
 __device__ __forceinline__ i32x2 ds_read_tr16(uint32_t lds_addr) {
   i32x2 r;
   asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(lds_addr) : "memory");
@@ -136,6 +137,14 @@ __device__ __forceinline__ i32x2 ds_read_tr8(uint32_t lds_addr) {
   asm volatile("ds_read_b64_tr_b8 %0, %1" : "=v"(r) : "v"(lds_addr) : "memory");
   return r;
 }
+__device__ __forceinline__ i32x4 ds_read_b128(uint32_t lds_addr) {
+  i32x4 r;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(lds_addr) : "memory");
+  return r;
+}
+__device__ __forceinline__ void lds_wait_4(i32x4 (&v)[4]) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]) : : "memory");
+}
 __device__ __forceinline__ void lds_wait_8(i32x2 (&v)[8]) {
   asm volatile("s_waitcnt lgkmcnt(0)"
                : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]), "+v"(v[7])
@@ -143,109 +152,190 @@ __device__ __forceinline__ void lds_wait_8(i32x2 (&v)[8]) {
                : "memory");
 }
 
+// A 16-byte global load the compiler does not track (so it adds no waits of
+// its own around the direct-to-LDS pipeline); vm_wait_all_4() waits for it.
+__device__ __forceinline__ i32x4 global_load_b128(const void* p) {
+  i32x4 r;
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(r) : "v"(p) : "memory");
+  return r;
+}
+__device__ __forceinline__ float global_load_f32(const float* p) {
+  float r;
+  asm volatile("global_load_dword %0, %1, off" : "=v"(r) : "v"(p) : "memory");
+  return r;
+}
+__device__ __forceinline__ void vm_wait_all_4(i32x4 (&v)[4], float& x, float& y) {
+  asm volatile("s_waitcnt vmcnt(0)" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(x), "+v"(y) : : "memory");
+}
+
 __device__ __forceinline__ uint16_t f32_to_bf16_bits(float x) {
   return __builtin_bit_cast(uint16_t, (__bf16)x);
 }
 
-// Enqueue the direct-to-LDS loads of one unit (its K tiles, then its V tiles)
-// into stage ui % NSTAGE of the wave's LDS region.  Each lane moves 16 bytes
-// per instruction; goff holds its swizzled source offsets inside a tile.
-template <bool FP8, int NSTAGE>
-__device__ __forceinline__ void issue_unit(char* wbase, int my_ids, int ui, const char* kpool, const char* vpool,
-                                           size_t block_stride, size_t head_tile, const int* goff) {
+__device__ __forceinline__ int clamp_ctx(int c, int max_ctx) { return c < 0 ? 0 : (c > max_ctx ? max_ctx : c); }
+
+template <bool FP8>
+__device__ __forceinline__ int units_of(int ctx) {
+  const int nb = (ctx + kBlock - 1) / kBlock;
+  return FP8 ? (nb + 1) >> 1 : nb;
+}
+
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
+  // vmcnt[3:0] | expcnt[6:4]=7 | lgkmcnt[11:8]=15 | vmcnt[5:4] in [15:14]).
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+// Ties the K registers to the wait just issued, so no consumer moves above it.
+__device__ __forceinline__ void dep4(i32x4 (&k)[4]) {
+  asm volatile("" : "+v"(k[0]), "+v"(k[1]), "+v"(k[2]), "+v"(k[3]));
+}
+
+// Wait until the K registers of the unit being computed have landed, given
+// how many later units are already in flight (each unit issues its 4 K loads,
+// then its V loads).
+template <int D, int LPU, int VLD>
+__device__ __forceinline__ void wait_k(int younger, i32x4 (&k)[4]) {
+  if (D >= 3 && younger >= 3) vm_wait<(D >= 3 ? VLD + 3 * LPU : 0)>();
+  else if (D >= 2 && younger == 2) vm_wait<(D >= 2 ? VLD + 2 * LPU : 0)>();
+  else if (younger == 1) vm_wait<VLD + LPU>();
+  else vm_wait<VLD>();
+  dep4(k);
+}
+// Wait until the V tiles of the unit being computed are in LDS.
+template <int D, int LPU>
+__device__ __forceinline__ void wait_v(int younger) {
+  if (D >= 3 && younger >= 3) vm_wait<(D >= 3 ? 3 * LPU : 0)>();
+  else if (D >= 2 && younger == 2) vm_wait<(D >= 2 ? 2 * LPU : 0)>();
+  else if (younger == 1) vm_wait<LPU>();
+  else vm_wait<0>();
+}
+
+// Enqueue one unit: its K tile rows straight into this lane's registers in
+// the MFMA A-operand layout (4 x 16 bytes per lane), then its V tiles into an
+// LDS stage with direct-to-LDS loads (16 bytes per lane per instruction,
+// chunk-swizzled per row).  tiles[] holds the flat tile index
+// (block id * Hkv + head) of each block of each unit of the slice.
+template <bool FP8>
+__device__ __forceinline__ void issue_unit(const int* tiles, int ui, const char* kpool, const char* vpool,
+                                           const int* goff, const int* kgoff, int kblk, char* vst, i32x4 (&kr)[4]) {
   constexpr int UB = FP8 ? 2 : 1;
   constexpr int TILE = FP8 ? 2048 : 4096;
-  constexpr int STAGE = 2 * UB * TILE;
   constexpr int DMA_PER_TILE = TILE / 1024;
-  char* st = wbase + (ui % NSTAGE) * STAGE;
+  int t[UB];
+  for (int b = 0; b < UB; ++b) t[b] = __builtin_amdgcn_readfirstlane(tiles[ui * UB + b]);
+  const int tk = (FP8 && kblk) ? t[UB - 1] : t[0];
+  const char* kbase = kpool + (size_t)tk * TILE;
+  for (int c = 0; c < 4; ++c) kr[c] = global_load_b128(kbase + kgoff[c]);
   for (int b = 0; b < UB; ++b) {
-    const int id = __builtin_amdgcn_readlane(my_ids, ui * UB + b);
-    const char* kt = kpool + (size_t)id * block_stride + head_tile;
+    const char* vt = vpool + (size_t)t[b] * TILE;
     for (int k = 0; k < DMA_PER_TILE; ++k)
-      __builtin_amdgcn_global_load_lds(kt + goff[k], (LDS_AS void*)(st + b * TILE + k * 1024), 16, 0, 0);
-  }
-  for (int b = 0; b < UB; ++b) {
-    const int id = __builtin_amdgcn_readlane(my_ids, ui * UB + b);
-    const char* vt = vpool + (size_t)id * block_stride + head_tile;
-    for (int k = 0; k < DMA_PER_TILE; ++k)
-      __builtin_amdgcn_global_load_lds(vt + goff[k], (LDS_AS void*)(st + UB * TILE + b * TILE + k * 1024), 16, 0,
-                                       0);
+      __builtin_amdgcn_global_load_lds(vt + goff[k], (LDS_AS void*)(vst + b * TILE + k * 1024), 16, 0, 0);
   }
 }
 
-template <bool FP8, int NW, int NSTAGE>
-__global__ __launch_bounds__(NW * 64) void paged_decode_partition_kernel(DecodeArgs a) {
+// D = units in flight ahead of the one being computed (1..3); the wave keeps
+// D + 1 register stages for K and D + 1 LDS stages for V.
+template <bool FP8, int D>
+__global__ __launch_bounds__(kWaves * 64) void paged_decode_stream_kernel(StreamArgs a) {
+  constexpr int NW = kWaves;
+  constexpr int NS = D + 1;
   constexpr int UB = FP8 ? 2 : 1;                // blocks per unit
   constexpr int TILE = FP8 ? 2048 : 4096;        // bytes of one (block, head) tile
-  constexpr int STAGE = 2 * UB * TILE;           // K tiles then V tiles
-  constexpr int DMA_PER_TILE = TILE / 1024;      // 64 lanes x 16 B per instruction
-  constexpr int LOADS_PER_UNIT = 2 * UB * DMA_PER_TILE;
-  constexpr int LOADS_V = UB * DMA_PER_TILE;
-  constexpr int MERGE_STRIDE = kHeadDim + 4;     // floats per head row in the merge area
-  static_assert(NW * NSTAGE * STAGE >= NW * 16 * 2 * 4 + NW * 16 * MERGE_STRIDE * 4, "merge area fits");
-  __shared__ __attribute__((aligned(1024))) char smem[NW * NSTAGE * STAGE];
+  constexpr int VSTAGE = UB * TILE;              // V tiles of one unit
+  constexpr int VLD = UB * (TILE / 1024);        // V load instructions per unit
+  constexpr int LPU = 4 + VLD;                   // vector-memory instructions per unit
+  __shared__ __attribute__((aligned(1024))) char vstages[NW * NS * VSTAGE];
+  __shared__ int tiles_lds[NW][kMaxUnitsPerWave * UB];
+  __shared__ int wave_sums[NW];
+  extern __shared__ int dyn[];                   // pre[B + 1] (unit prefix), ctxs[B]
 
-  const int p = blockIdx.x, g = blockIdx.y, s = blockIdx.z;
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int G = a.group;
+  const int B = a.batch, Hkv = a.hkv, G = a.group;
   const int li = lane & 15;  // MFMA column (head) / row index
   const int lj = lane >> 4;  // 16-lane row of the wave
+  int* pre = dyn;
+  int* ctxs = dyn + B + 1;
 
-  int ctx = a.context_lens[s];
-  ctx = ctx < 0 ? 0 : (ctx > a.max_ctx ? a.max_ctx : ctx);
-  const int P = a.part_tokens;
-  if (ctx == 0) {
-    if (p == 0) {  // empty sequence: zero output rows of this KV head's query heads
-      for (int idx = threadIdx.x; idx < G * kHeadDim; idx += NW * 64) {
-        const size_t o = ((size_t)s * a.hq + (size_t)g * G) * kHeadDim + idx;
-        if (a.out_fp32) ((float*)a.out)[o] = 0.f;
-        else ((uint16_t*)a.out)[o] = 0;
+  // ---- 1. prefix of units over sequences (every workgroup computes it) ----
+  {
+    const int T = NW * 64, tid = threadIdx.x;
+    const int per = (B + T - 1) / T;
+    int local = 0;
+    for (int k = 0; k < per; ++k) {
+      const int s = tid * per + k;
+      if (s < B) {
+        const int c = clamp_ctx(a.context_lens[s], a.max_ctx);
+        ctxs[s] = c;
+        local += units_of<FP8>(c);
       }
     }
-    return;
-  }
-  const int n_parts = (ctx + P - 1) / P;
-  if (p >= n_parts) return;
-  const int tok_begin = p * P;
-  const int tok_end = min(ctx, tok_begin + P);
-  const int kb0 = tok_begin / kBlock;
-  const int nb = (tok_end - tok_begin + kBlock - 1) / kBlock;
-  const int n_units = (nb + UB - 1) / UB;
-  const int my_units = n_units > w ? (n_units - w + NW - 1) / NW : 0;
-
-  // Block ids of this wave's units, one per lane: lane L <-> (unit L / UB, block L % UB).
-  int my_ids = 0;
-  {
-    const int L = lane;
-    if (L < my_units * UB) {
-      int bi = kb0 + (w + NW * (L / UB)) * UB + (L % UB);
-      if (bi >= kb0 + nb) bi -= 1;  // absent second block of a unit: reload the first (masked later)
-      int id = a.block_tables[(size_t)s * a.max_blocks_per_seq + bi];
-      my_ids = id < 0 ? 0 : (id > a.num_blocks_m1 ? a.num_blocks_m1 : id);
+    int incl = local;
+    for (int off = 1; off < 64; off <<= 1) {
+      const int v = __shfl_up(incl, off);
+      if (lane >= off) incl += v;
     }
-  }
-
-  // Q as the MFMA B operand: lane (li, lj) holds head li, 8 head-dim values per chunk c.
-  bf16x8 qop[4];
-  {
-    const int h = g * G + li;
-    for (int c = 0; c < 4; ++c) {
-      const int d = FP8 ? 64 * (c >> 1) + 16 * lj + 8 * (c & 1) : 32 * c + 8 * lj;
-      if (li < G) {
-        qop[c] = *(const bf16x8*)(a.q + ((size_t)s * a.hq + h) * kHeadDim + d);
-      } else {
-        for (int e = 0; e < 8; ++e) qop[c][e] = (__bf16)0.f;
+    if (lane == 63) wave_sums[w] = incl;
+    __syncthreads();
+    int run = incl - local;
+    for (int k = 0; k < w; ++k) run += wave_sums[k];
+    for (int k = 0; k < per; ++k) {
+      const int s = tid * per + k;
+      if (s < B) {
+        pre[s] = run;
+        run += units_of<FP8>(ctxs[s]);
       }
     }
+    if (tid == T - 1) pre[B] = run;
+    __syncthreads();
   }
-  float cs = a.qk_scale_log2;
-  if constexpr (FP8) cs *= a.k_scale[g];
+  const int U = Hkv * pre[B];
+  const int TW = gridDim.x * NW;
+  int C = (U + TW - 1) / TW;
+  if (C < a.min_chunk) C = a.min_chunk;
+  if (blockIdx.x == 0) {  // the merge kernel needs the prefix and the slice length
+    for (int s = threadIdx.x; s <= B; s += NW * 64) a.plan[s] = pre[s];
+    if (threadIdx.x == 0) a.plan[B + 1] = C;
+  }
+  const int gw = blockIdx.x * NW + w;
+  const int u0 = gw * C;
+  const int u1 = min(u0 + C, U);
+  if (u0 >= u1) {  // no work: no segment to terminate
+    if (lane == 0) *(i32x4*)(a.hdr + 4 * gw) = i32x4{0, 0, 0, 0};
+    return;  // no barrier follows: waves are independent from here on
+  }
+  const int n = u1 - u0;
 
-  // Per-lane byte offsets: global (inside a tile) for each DMA instruction, and
-  // LDS (inside a stage) for the MFMA-layout K reads and the transposing V reads.
-  int goff[DMA_PER_TILE];
-  for (int k = 0; k < DMA_PER_TILE; ++k) {
+  // ---- 2. tile indices of this wave's units into LDS ----
+  int* tiles = tiles_lds[w];
+  for (int i = lane; i < n; i += 64) {
+    const int u = u0 + i;
+    int lo = 0, hi = B - 1;  // largest s with Hkv * pre[s] <= u
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (Hkv * pre[mid] <= u) lo = mid;
+      else hi = mid - 1;
+    }
+    const int s = lo;
+    const int nus = pre[s + 1] - pre[s];
+    const int r = u - Hkv * pre[s];
+    const int g = r / nus;
+    const int j = r - g * nus;
+    const int nb = (ctxs[s] + kBlock - 1) / kBlock;
+    for (int b = 0; b < UB; ++b) {
+      int blk = j * UB + b;
+      if (blk >= nb) blk = j * UB;  // absent second block of an fp8 unit: reload the first (masked later)
+      int id = a.block_tables[(size_t)s * a.max_blocks_per_seq + blk];
+      id = id < 0 ? 0 : (id > a.num_blocks_m1 ? a.num_blocks_m1 : id);
+      tiles[i * UB + b] = id * Hkv + g;
+    }
+  }
+
+  // ---- 3. per-lane offsets ----
+  int goff[TILE / 1024];  // V: source offset inside a tile for each direct-to-LDS instruction
+  for (int k = 0; k < TILE / 1024; ++k) {
     if constexpr (FP8) {
       const int row = 8 * k + (lane >> 3);
       goff[k] = row * 128 + 16 * ((lane & 7) ^ swz_fp8(row));
@@ -254,230 +344,322 @@ __global__ __launch_bounds__(NW * 64) void paged_decode_partition_kernel(DecodeA
       goff[k] = row * 256 + 16 * ((lane & 15) ^ swz_bf16(row));
     }
   }
-  int koff[4];  // bf16: chunk c ; fp8: (group q, half h) -> index 2q + h
-  int voff[8];
+  int kgoff[4];   // K: bf16 chunk c -> row li, bytes 64c + 16lj ; fp8 (group q, half h) -> 2q + h
+  int kblk = 0;   // fp8: which block of the unit this lane's K rows come from
+  int voff[8];    // V: transposing-read offsets inside a V stage
   if constexpr (FP8) {
+    kblk = li >> 3;
     for (int qg = 0; qg < 2; ++qg)
       for (int hh = 0; hh < 2; ++hh) {
         const int tau = 8 * (li >> 2) + 4 * qg + (li & 3);
-        const int b = tau >> 4, r = tau & 15;
-        koff[2 * qg + hh] = b * TILE + r * 128 + 16 * ((4 * hh + lj) ^ swz_fp8(r));
+        kgoff[2 * qg + hh] = (tau & 15) * 128 + 16 * (4 * hh + lj);
       }
-    for (int n = 0; n < 8; ++n) {
+    for (int nn = 0; nn < 8; ++nn) {
       const int tau = 8 * lj + (li >> 1);
       const int b = tau >> 4, r = tau & 15;
-      voff[n] = UB * TILE + b * TILE + r * 128 + 16 * (n ^ swz_fp8(r)) + 8 * (lane & 1);
+      voff[nn] = b * TILE + r * 128 + 16 * (nn ^ swz_fp8(r)) + 8 * (lane & 1);
     }
   } else {
-    for (int c = 0; c < 4; ++c) koff[c] = li * 256 + 16 * ((4 * c + lj) ^ swz_bf16(li));
-    for (int n = 0; n < 8; ++n) {
+    for (int c = 0; c < 4; ++c) kgoff[c] = li * 256 + 16 * (4 * c + lj);
+    for (int nn = 0; nn < 8; ++nn) {
       const int row = 4 * lj + (li >> 2);
-      voff[n] = TILE + row * 256 + 16 * ((2 * n + ((lane & 3) >> 1)) ^ swz_bf16(row)) + 8 * (lane & 1);
+      voff[nn] = row * 256 + 16 * ((2 * nn + ((lane & 3) >> 1)) ^ swz_bf16(row)) + 8 * (lane & 1);
     }
   }
 
-  char* const wbase = smem + w * NSTAGE * STAGE;
-  const size_t head_tile = (size_t)g * TILE;
-  const size_t block_stride = (size_t)a.hkv * TILE;
+  // ---- 4. walk the slice ----
+  char* const wv = vstages + w * NS * VSTAGE;
+  // compute-side position (uniform): segment (s, g), unit j inside it
+  int cs_s, cs_g, cs_j, cs_nus;
+  {
+    int lo = 0, hi = B - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (Hkv * pre[mid] <= u0) lo = mid;
+      else hi = mid - 1;
+    }
+    cs_s = __builtin_amdgcn_readfirstlane(lo);
+    cs_nus = __builtin_amdgcn_readfirstlane(pre[cs_s + 1] - pre[cs_s]);
+    const int r = u0 - Hkv * pre[cs_s];
+    cs_g = __builtin_amdgcn_readfirstlane(r / cs_nus);
+    cs_j = __builtin_amdgcn_readfirstlane(r - cs_g * cs_nus);
+    // this wave terminates a split segment when its first piece continues a
+    // segment begun by an earlier wave and the segment ends inside this slice
+    const bool term = cs_j > 0 && cs_nus - cs_j <= n;
+    if (lane == 0)
+      *(i32x4*)(a.hdr + 4 * gw) = term ? i32x4{cs_s, cs_g, u0 - cs_j, cs_nus} : i32x4{0, 0, 0, 0};
+  }
 
-  float m_run = -INFINITY;  // running max (log2 units) of head li
-  float l_part = 0.f;       // this lane's share of the running sum of head li
+  i32x4 kreg[NS][4];
+#pragma unroll
+  for (int S = 0; S < D; ++S)
+    if (S < n) issue_unit<FP8>(tiles, S, a.k, a.v, goff, kgoff, kblk, wv + S * VSTAGE, kreg[S]);
+
+  bf16x8 qop[4];
+  float m_run = -INFINITY, l_part = 0.f, cscale = 0.f, vsc = 1.0f;
   f32x4 acc[8];
-  for (int n = 0; n < 8; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+  int piece_j0 = 0, ctx_s = 0;
+  bool piece_first = true;
 
-  const int pro = min(NSTAGE - 1, my_units);
-  for (int ui = 0; ui < pro; ++ui)
-    issue_unit<FP8, NSTAGE>(wbase, my_ids, ui, a.k, a.v, block_stride, head_tile, goff);
-
-  for (int ui = 0; ui < my_units; ++ui) {
-    if (ui + NSTAGE - 1 < my_units) {
-      __builtin_amdgcn_s_waitcnt((7 << 4) | (0 << 8) | (15) | (3 << 14));  // lgkmcnt(0): stage reads done
-      issue_unit<FP8, NSTAGE>(wbase, my_ids, ui + NSTAGE - 1, a.k, a.v, block_stride, head_tile, goff);
-    }
-    const int younger = min(NSTAGE - 1, my_units - 1 - ui);
-    const char* st = wbase + (ui % NSTAGE) * STAGE;
-    const uint32_t st_lds = (uint32_t)(uintptr_t)(const LDS_AS char*)st;
-    const int unit_tok0 = (kb0 + (w + NW * ui) * UB) * kBlock;
-    const bool ragged = unit_tok0 + UB * kBlock > tok_end;
-
-    wait_vmcnt(younger * LOADS_PER_UNIT + LOADS_V);  // K tiles of this unit have landed
-
-    float z[2 * UB * 2];  // bf16: 4 scores (tokens 4lj+r); fp8: 8 scores (tokens 8lj+e)
-    if constexpr (FP8) {
-      for (int qg = 0; qg < 2; ++qg) {
-        f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
-        for (int hh = 0; hh < 2; ++hh) {
-          const i32x4 raw = *(const LDS_AS i32x4*)(st + koff[2 * qg + hh]);
-          const bf16x8 k0 = fp8x8_to_bf16(raw[0], raw[1]);
-          const bf16x8 k1 = fp8x8_to_bf16(raw[2], raw[3]);
-          sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qop[2 * hh], sacc, 0, 0, 0);
-          sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qop[2 * hh + 1], sacc, 0, 0, 0);
+  for (int base = 0; base < n; base += NS) {
+#pragma unroll
+    for (int S = 0; S < NS; ++S) {
+      const int ui = base + S;
+      if (ui >= n) break;
+      if (ui + D < n) {
+        __builtin_amdgcn_s_waitcnt((7 << 4) | (0 << 8) | (15) | (3 << 14));  // lgkmcnt(0): stage reads done
+        issue_unit<FP8>(tiles, ui + D, a.k, a.v, goff, kgoff, kblk, wv + ((S + D) % NS) * VSTAGE,
+                        kreg[(S + D) % NS]);
+      }
+      if (ui == 0 || cs_j == 0) {  // a new piece starts: its query group, fresh softmax state
+        piece_first = ui == 0;
+        piece_j0 = cs_j;
+        ctx_s = __builtin_amdgcn_readfirstlane(ctxs[cs_s]);
+        // lanes of padding heads (li >= G) load head g*G and are zeroed below
+        const uint16_t* qrow = a.q + ((size_t)cs_s * a.hq + cs_g * G + (li < G ? li : 0)) * kHeadDim;
+        i32x4 qraw[4];
+        for (int c = 0; c < 4; ++c)
+          qraw[c] = global_load_b128(qrow + (FP8 ? 64 * (c >> 1) + 16 * lj + 8 * (c & 1) : 32 * c + 8 * lj));
+        float ksc = 1.0f;
+        vsc = 1.0f;
+        if constexpr (FP8) {
+          ksc = global_load_f32(a.k_scale + cs_g);
+          vsc = global_load_f32(a.v_scale + cs_g);
         }
-        for (int r = 0; r < 4; ++r) z[4 * qg + r] = sacc[r] * cs;
+        vm_wait_all_4(qraw, ksc, vsc);  // drains this wave's loads in flight too (once per piece)
+        for (int c = 0; c < 4; ++c) {
+          if (li < G) {
+            qop[c] = __builtin_bit_cast(bf16x8, qraw[c]);
+          } else {
+            for (int e = 0; e < 8; ++e) qop[c][e] = (__bf16)0.f;
+          }
+        }
+        cscale = a.qk_scale_log2 * ksc;
+        m_run = -INFINITY;
+        l_part = 0.f;
+        for (int nn = 0; nn < 8; ++nn) acc[nn] = f32x4{0.f, 0.f, 0.f, 0.f};
       }
-      if (ragged)
-        for (int e = 0; e < 8; ++e)
-          if (unit_tok0 + 8 * lj + e >= tok_end) z[e] = -INFINITY;
-    } else {
-      f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
-      for (int c = 0; c < 4; ++c) {
-        const bf16x8 kop = *(const LDS_AS bf16x8*)(st + koff[c]);
-        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[c], sacc, 0, 0, 0);
-      }
-      for (int r = 0; r < 4; ++r) z[r] = sacc[r] * cs;
-      if (ragged)
-        for (int r = 0; r < 4; ++r)
-          if (unit_tok0 + 4 * lj + r >= tok_end) z[r] = -INFINITY;
-    }
+      const int younger = min(D, n - 1 - ui);
+      const uint32_t vst = (uint32_t)(uintptr_t)(const LDS_AS char*)(wv + S * VSTAGE);
+      const int unit_tok0 = cs_j * UB * kBlock;
+      const bool ragged = unit_tok0 + UB * kBlock > ctx_s;
 
-    // online softmax (base 2) for head li over this unit's tokens
-    constexpr int NZ = FP8 ? 8 : 4;
-    float bmax = z[0];
-    for (int e = 1; e < NZ; ++e) bmax = fmaxf(bmax, z[e]);
-    bmax = xor_max(bmax);
-    const float m_new = fmaxf(m_run, bmax);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
-    __bf16 pb[NZ];
-    float psum = 0.f;
-    for (int e = 0; e < NZ; ++e) {
-      pb[e] = (__bf16)__builtin_amdgcn_exp2f(z[e] - m_new);
-      psum += (float)pb[e];
-    }
-    l_part = l_part * alpha + psum;
-    for (int n = 0; n < 8; ++n) acc[n] *= alpha;
+      wait_k<D, LPU, VLD>(younger, kreg[S]);  // K rows of this unit are in registers
 
-    wait_vmcnt(younger * LOADS_PER_UNIT);  // V tiles of this unit have landed
-
-    if constexpr (FP8) {
-      bf16x8 pop;
-      for (int e = 0; e < 8; ++e) pop[e] = pb[e];
-      i32x2 raw[8];
-      for (int n = 0; n < 8; ++n) raw[n] = ds_read_tr8(st_lds + voff[n]);
-      lds_wait_8(raw);
-      for (int n = 0; n < 8; ++n) {
-        bf16x8 vop = fp8x8_to_bf16(raw[n][0], raw[n][1]);
+      constexpr int NZ = FP8 ? 8 : 4;  // scores per lane: bf16 tokens 4lj+r ; fp8 tokens 8lj+e
+      float z[NZ];
+      if constexpr (FP8) {
+        for (int qg = 0; qg < 2; ++qg) {
+          f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
+          for (int hh = 0; hh < 2; ++hh) {
+            const i32x4 raw = kreg[S][2 * qg + hh];
+            const bf16x8 k0 = fp8x8_to_bf16(raw[0], raw[1]);
+            const bf16x8 k1 = fp8x8_to_bf16(raw[2], raw[3]);
+            sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qop[2 * hh], sacc, 0, 0, 0);
+            sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qop[2 * hh + 1], sacc, 0, 0, 0);
+          }
+          for (int r = 0; r < 4; ++r) z[4 * qg + r] = sacc[r] * cscale;
+        }
         if (ragged)
           for (int e = 0; e < 8; ++e)
-            if (unit_tok0 + 8 * lj + e >= tok_end) vop[e] = (__bf16)0.f;
-        acc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop, acc[n], 0, 0, 0);
-      }
-    } else {
-      bf16x4 pop;
-      for (int e = 0; e < 4; ++e) pop[e] = pb[e];
-      i32x2 raw[8];
-      for (int n = 0; n < 8; ++n) raw[n] = ds_read_tr16(st_lds + voff[n]);
-      lds_wait_8(raw);
-      for (int n = 0; n < 8; ++n) {
-        bf16x4 vop = __builtin_bit_cast(bf16x4, raw[n]);
+            if (unit_tok0 + 8 * lj + e >= ctx_s) z[e] = -INFINITY;
+      } else {
+        f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
+        for (int c = 0; c < 4; ++c)
+          sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kreg[S][c]), qop[c], sacc, 0, 0,
+                                                         0);
+        for (int r = 0; r < 4; ++r) z[r] = sacc[r] * cscale;
         if (ragged)
-          for (int e = 0; e < 4; ++e)
-            if (unit_tok0 + 4 * lj + e >= tok_end) vop[e] = (__bf16)0.f;
-        acc[n] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vop, pop, acc[n], 0, 0, 0);
+          for (int r = 0; r < 4; ++r)
+            if (unit_tok0 + 4 * lj + r >= ctx_s) z[r] = -INFINITY;
+      }
+
+      // online softmax (base 2) for head li over this unit's tokens
+      float bmax = z[0];
+      for (int e = 1; e < NZ; ++e) bmax = fmaxf(bmax, z[e]);
+      bmax = xor_max(bmax);
+      const float m_new = fmaxf(m_run, bmax);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      __bf16 pb[NZ];
+      float psum = 0.f;
+      for (int e = 0; e < NZ; ++e) {
+        pb[e] = (__bf16)__builtin_amdgcn_exp2f(z[e] - m_new);
+        psum += (float)pb[e];
+      }
+      l_part = l_part * alpha + psum;
+      for (int nn = 0; nn < 8; ++nn) acc[nn] *= alpha;
+
+      wait_v<D, LPU>(younger);  // V tiles of this unit are in LDS
+
+      if constexpr (FP8) {
+        bf16x8 pop;
+        for (int e = 0; e < 8; ++e) pop[e] = pb[e];
+        i32x2 raw[8];
+        for (int nn = 0; nn < 8; ++nn) raw[nn] = ds_read_tr8(vst + voff[nn]);
+        lds_wait_8(raw);
+        for (int nn = 0; nn < 8; ++nn) {
+          bf16x8 vop = fp8x8_to_bf16(raw[nn][0], raw[nn][1]);
+          if (ragged)
+            for (int e = 0; e < 8; ++e)
+              if (unit_tok0 + 8 * lj + e >= ctx_s) vop[e] = (__bf16)0.f;
+          acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop, acc[nn], 0, 0, 0);
+        }
+      } else {
+        bf16x4 pop;
+        for (int e = 0; e < 4; ++e) pop[e] = pb[e];
+        i32x2 raw[8];
+        for (int nn = 0; nn < 8; ++nn) raw[nn] = ds_read_tr16(vst + voff[nn]);
+        lds_wait_8(raw);
+        for (int nn = 0; nn < 8; ++nn) {
+          bf16x4 vop = __builtin_bit_cast(bf16x4, raw[nn]);
+          if (ragged)
+            for (int e = 0; e < 4; ++e)
+              if (unit_tok0 + 4 * lj + e >= ctx_s) vop[e] = (__bf16)0.f;
+          acc[nn] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vop, pop, acc[nn], 0, 0, 0);
+        }
+      }
+
+      // ---- end of a piece: write the result or a partial record ----
+      const bool seg_end = cs_j == cs_nus - 1;
+      if (seg_end || ui == n - 1) {
+        const float l_tot = xor_sum(l_part);
+        const float inv = vsc / l_tot;
+        if (li < G) {
+          if (piece_j0 == 0 && seg_end) {  // the whole segment: final output
+            const size_t row = ((size_t)cs_s * a.hq + cs_g * G + li) * kHeadDim;
+            for (int nn = 0; nn < 8; ++nn) {
+              const f32x4 o = acc[nn] * inv;
+              const size_t off = row + 16 * nn + 4 * lj;
+              if (a.out_fp32) {
+                *(f32x4*)((float*)a.out + off) = o;
+              } else {
+                u16x4 ob;
+                for (int e = 0; e < 4; ++e) ob[e] = f32_to_bf16_bits(o[e]);
+                *(u16x4*)((uint16_t*)a.out + off) = ob;
+              }
+            }
+          } else {  // a piece of a segment cut by slice boundaries
+            const size_t rec = (size_t)gw * 2 + (piece_first ? 0 : 1);
+            float* ro = a.rec_o + (rec * G + li) * kHeadDim;
+            for (int nn = 0; nn < 8; ++nn) *(f32x4*)(ro + 16 * nn + 4 * lj) = acc[nn] * inv;
+            if (lj == 0) {
+              a.rec_ml[(rec * G + li) * 2 + 0] = m_run;
+              a.rec_ml[(rec * G + li) * 2 + 1] = l_tot;
+            }
+          }
+        }
+      }
+      // advance the compute-side position
+      if (ui + 1 < n) {
+        if (++cs_j == cs_nus) {
+          cs_j = 0;
+          if (++cs_g == Hkv) {
+            cs_g = 0;
+            do {
+              ++cs_s;
+            } while (cs_s < B - 1 && pre[cs_s + 1] == pre[cs_s]);  // skip empty sequences (bounded)
+            cs_s = __builtin_amdgcn_readfirstlane(cs_s);
+          }
+          cs_nus = __builtin_amdgcn_readfirstlane(pre[cs_s + 1] - pre[cs_s]);
+        }
       }
     }
   }
+}
 
-  // ---- merge the NW waves of this workgroup through LDS ----
-  const float l_wave = xor_sum(l_part);
-  __syncthreads();  // every wave is done with its stages
-  float* ml = (float*)smem;                      // [NW][16][2]
-  float* oacc = (float*)smem + NW * 16 * 2;      // [NW][16][MERGE_STRIDE]
-  if (lj == 0) {
-    ml[(w * 16 + li) * 2 + 0] = m_run;
-    ml[(w * 16 + li) * 2 + 1] = l_wave;
-  }
-  __syncthreads();
-  float M = -INFINITY;
-  for (int ww = 0; ww < NW; ++ww) M = fmaxf(M, ml[(ww * 16 + li) * 2]);
-  const float f_self = my_units > 0 ? __builtin_amdgcn_exp2f(m_run - M) : 0.f;
-  for (int n = 0; n < 8; ++n) {
-    f32x4 o = acc[n] * f_self;
-    *(f32x4*)(oacc + (w * 16 + li) * MERGE_STRIDE + 16 * n + 4 * lj) = o;
-  }
-  __syncthreads();
-
-  float vsc = 1.0f;
-  if constexpr (FP8) vsc = a.v_scale[g];
-  const bool single = n_parts == 1;
-  for (int idx = threadIdx.x; idx < G * 32; idx += NW * 64) {
-    const int i = idx >> 5;
-    const int d = (idx & 31) * 4;
-    float Mi = -INFINITY;
-    for (int ww = 0; ww < NW; ++ww) Mi = fmaxf(Mi, ml[(ww * 16 + i) * 2]);
-    float Li = 0.f;
-    f32x4 o = {0.f, 0.f, 0.f, 0.f};
-    for (int ww = 0; ww < NW; ++ww) {
-      const float mw = ml[(ww * 16 + i) * 2];
-      const float f = mw == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw - Mi);
-      Li += ml[(ww * 16 + i) * 2 + 1] * f;
-      o += *(const f32x4*)(oacc + (ww * 16 + i) * MERGE_STRIDE + d);
+// Log-sum-exp merge of the pieces of every segment cut by slice boundaries,
+// and zero rows for empty sequences.  One workgroup per wave of the stream
+// kernel: workgroup k merges the segment that wave k terminates (if any).
+// That segment covers units [a0, a0 + nus); slices have length C, so its
+// pieces come from waves k0 = a0 / C .. k: wave k0's last piece (record slot
+// 1 if that wave began inside an earlier segment, else slot 0) and the first
+// piece (slot 0) of every later wave.  256 threads = record groups x G heads
+// x 8 lanes of 16 head-dim values; each group folds its records with a
+// running log-sum-exp, and the groups are combined in LDS:
+// M = max_p m_p, w_p = l_p 2^(m_p - M), out = sum_p w_p o_p / sum_p w_p.
+__global__ __launch_bounds__(256) void paged_decode_merge_kernel(StreamArgs a) {
+  const int k = blockIdx.x;
+  const int G = a.group, B = a.batch;
+  const int tid = threadIdx.x;
+  for (int s = k; s < B; s += gridDim.x) {  // empty sequences: zero rows
+    if (a.plan[s + 1] == a.plan[s]) {
+      for (int idx = tid; idx < a.hq * 32; idx += 256) {
+        const size_t o = (size_t)s * a.hq * kHeadDim + (size_t)idx * 4;
+        if (a.out_fp32) *(f32x4*)((float*)a.out + o) = f32x4{0.f, 0.f, 0.f, 0.f};
+        else *(u16x4*)((uint16_t*)a.out + o) = u16x4{0, 0, 0, 0};
+      }
     }
-    const float inv = vsc / Li;
-    o *= inv;
-    const int h = g * G + i;
-    if (single) {
-      const size_t off = ((size_t)s * a.hq + h) * kHeadDim + d;
+  }
+  const i32x4 h = *(const i32x4*)(a.hdr + 4 * k);
+  const int s = h[0], g = h[1], a0 = h[2], nus = h[3];
+  if (nus == 0) return;  // wave k terminates no split segment
+  const int C = a.plan[B + 1];
+  const int k0 = a0 / C;
+  const int first_slot = k0 * 2 + (a0 > k0 * C ? 1 : 0);
+  const int nrec = k - k0 + 1;
+  const int groups = 256 / (8 * G);             // G <= 16: at least 2 groups
+  const int grp = tid / (8 * G);
+  const int i = (tid >> 3) % G;                  // head inside the group
+  const int d0 = (tid & 7) * 16;                 // 16 head-dim values per lane
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4 acc[4] = {};
+  if (grp < groups) {
+    for (int r = grp; r < nrec; r += groups) {
+      const size_t rec = r == 0 ? (size_t)first_slot : (size_t)(k0 + r) * 2;
+      const float* ml = a.rec_ml + (rec * G + i) * 2;
+      const float m = ml[0], l = ml[1];
+      const f32x4* o = (const f32x4*)(a.rec_o + (rec * G + i) * kHeadDim + d0);
+      const float m_new = fmaxf(m_run, m);
+      const float c_old = __builtin_amdgcn_exp2f(m_run - m_new);
+      const float c_new = l * __builtin_amdgcn_exp2f(m - m_new);
+      for (int e = 0; e < 4; ++e) acc[e] = acc[e] * c_old + o[e] * c_new;
+      l_run = l_run * c_old + c_new;
+      m_run = m_new;
+    }
+  }
+  __shared__ float sm[32][16], sl[32][16];
+  __shared__ f32x4 sacc[256][4];
+  if (grp < groups) {
+    if ((tid & 7) == 0) {
+      sm[grp][i] = m_run;
+      sl[grp][i] = l_run;
+    }
+    for (int e = 0; e < 4; ++e) sacc[tid][e] = acc[e];
+  }
+  __syncthreads();
+  if (grp == 0) {
+    float M = -INFINITY;
+    for (int q = 0; q < groups; ++q) M = fmaxf(M, sm[q][i]);
+    float L = 0.f;
+    f32x4 o[4] = {};
+    for (int q = 0; q < groups; ++q) {
+      const float c = sm[q][i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sm[q][i] - M);
+      L += sl[q][i] * c;
+      for (int e = 0; e < 4; ++e) o[e] += sacc[q * 8 * G + tid][e] * c;
+    }
+    const float inv = 1.0f / L;
+    const size_t orow = ((size_t)s * a.hq + (size_t)g * G + i) * kHeadDim + d0;
+    for (int e = 0; e < 4; ++e) {
+      const f32x4 v = o[e] * inv;
       if (a.out_fp32) {
-        *(f32x4*)((float*)a.out + off) = o;
+        *(f32x4*)((float*)a.out + orow + 4 * e) = v;
       } else {
         u16x4 ob;
-        for (int e = 0; e < 4; ++e) ob[e] = f32_to_bf16_bits(o[e]);
-        *(u16x4*)((uint16_t*)a.out + off) = ob;
-      }
-    } else {
-      const size_t row = ((size_t)s * a.hq + h) * a.max_parts + p;
-      *(f32x4*)(a.part_o + row * kHeadDim + d) = o;
-      if (d == 0) {
-        a.part_ml[row * 2 + 0] = Mi;
-        a.part_ml[row * 2 + 1] = Li;
+        for (int q = 0; q < 4; ++q) ob[q] = f32_to_bf16_bits(v[q]);
+        *(u16x4*)((uint16_t*)a.out + orow + 4 * e) = ob;
       }
     }
   }
 }
 
-// Log-sum-exp merge of the partition partials of each (sequence, KV head):
-// M = max_p m_p, w_p = l_p 2^(m_p - M), out = sum_p w_p o_p / sum_p w_p.
-__global__ __launch_bounds__(256) void paged_decode_merge_kernel(DecodeArgs a) {
-  const int g = blockIdx.x, s = blockIdx.y;
-  int ctx = a.context_lens[s];
-  ctx = ctx < 0 ? 0 : (ctx > a.max_ctx ? a.max_ctx : ctx);
-  const int n_parts = (ctx + a.part_tokens - 1) / a.part_tokens;
-  if (n_parts <= 1) return;  // written directly by the partition kernel
-  const int G = a.group;
-  for (int idx = threadIdx.x; idx < G * 32; idx += 256) {
-    const int i = idx >> 5;
-    const int d = (idx & 31) * 4;
-    const int h = g * G + i;
-    const size_t row0 = ((size_t)s * a.hq + h) * a.max_parts;
-    float M = -INFINITY;
-    for (int pp = 0; pp < n_parts; ++pp) M = fmaxf(M, a.part_ml[(row0 + pp) * 2]);
-    float L = 0.f;
-    f32x4 o = {0.f, 0.f, 0.f, 0.f};
-    for (int pp = 0; pp < n_parts; ++pp) {
-      const float wgt = a.part_ml[(row0 + pp) * 2 + 1] * __builtin_amdgcn_exp2f(a.part_ml[(row0 + pp) * 2] - M);
-      L += wgt;
-      o += wgt * *(const f32x4*)(a.part_o + (row0 + pp) * kHeadDim + d);
-    }
-    o *= 1.0f / L;
-    const size_t off = ((size_t)s * a.hq + h) * kHeadDim + d;
-    if (a.out_fp32) {
-      *(f32x4*)((float*)a.out + off) = o;
-    } else {
-      u16x4 ob;
-      for (int e = 0; e < 4; ++e) ob[e] = f32_to_bf16_bits(o[e]);
-      *(u16x4*)((uint16_t*)a.out + off) = ob;
-    }
-  }
-}
-
-// The instantiations the launcher dispatches to (bf16 / fp8 KV, 2-4 stages).
-template __global__ void paged_decode_partition_kernel<false, 4, 2>(DecodeArgs);
-template __global__ void paged_decode_partition_kernel<true, 4, 2>(DecodeArgs);
-template __global__ void paged_decode_partition_kernel<false, 4, 3>(DecodeArgs);
-template __global__ void paged_decode_partition_kernel<true, 4, 3>(DecodeArgs);
-template __global__ void paged_decode_partition_kernel<false, 4, 4>(DecodeArgs);
-template __global__ void paged_decode_partition_kernel<true, 4, 4>(DecodeArgs);
+// The instantiations the launcher dispatches to (bf16 / fp8 KV, 1-3 units in flight).
+template __global__ void paged_decode_stream_kernel<false, 1>(StreamArgs);
+template __global__ void paged_decode_stream_kernel<true, 1>(StreamArgs);
+template __global__ void paged_decode_stream_kernel<false, 2>(StreamArgs);
+template __global__ void paged_decode_stream_kernel<true, 2>(StreamArgs);
+template __global__ void paged_decode_stream_kernel<false, 3>(StreamArgs);
+template __global__ void paged_decode_stream_kernel<true, 3>(StreamArgs);
 
 }  // namespace dpool_hip
 
@@ -485,22 +667,79 @@ namespace {
 
 using namespace dpool_hip;
 
-constexpr int kWaves = 4;
+constexpr int kMaxBatchInLds = 4096;  // the unit prefix of the batch is kept in LDS
+constexpr size_t kLdsBytes = 160 * 1024;
 
-int default_partition(const dp_decode_shape* sh) {
-  const int unit = sh->kv_dtype == DP_KV_FP8_E4M3 ? 32 : 16;
-  int P = 512;
-  const int need = ((sh->max_context_len + unit - 1) / unit) * unit;
-  if (need > 0 && need < P) P = need;  // one partition covers every sequence
-  return std::max(P, unit);
+// Compute units of the current device (cached per device); 256 when no device
+// is visible, so that host-only callers still get a deterministic answer.
+int device_cus(int* dev_out) {
+  static std::mutex mu;
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+    (void)hipGetLastError();
+    *dev_out = -1;
+    return 256;
+  }
+  *dev_out = dev;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!cached[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) {
+      (void)hipGetLastError();
+      n = 256;
+    }
+    cached[dev] = n;
+  }
+  return cached[dev];
 }
 
-int default_stages(const dp_decode_shape*) { return 2; }
+const void* stream_kernel(bool fp8, int d) {
+  switch (d * 2 + (fp8 ? 1 : 0)) {
+    case 2: return (const void*)paged_decode_stream_kernel<false, 1>;
+    case 3: return (const void*)paged_decode_stream_kernel<true, 1>;
+    case 4: return (const void*)paged_decode_stream_kernel<false, 2>;
+    case 5: return (const void*)paged_decode_stream_kernel<true, 2>;
+    case 6: return (const void*)paged_decode_stream_kernel<false, 3>;
+    default: return (const void*)paged_decode_stream_kernel<true, 3>;
+  }
+}
+
+// Workgroups of the stream kernel one compute unit holds at once, limited by
+// registers (runtime occupancy query, cached) and by LDS.  Without a device,
+// only the LDS limit applies.
+int blocks_per_cu(int dev, bool fp8, int d, size_t lds_bytes) {
+  static std::mutex mu;
+  static int cached[64][2][4] = {};
+  int by_lds = (int)(kLdsBytes / lds_bytes);
+  if (dev < 0) return std::max(1, std::min(by_lds, 2));
+  int occ;
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    occ = cached[dev][fp8 ? 1 : 0][d];
+    if (!occ) {
+      int n = 0;
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, stream_kernel(fp8, d), kWaves * 64, 0) != hipSuccess ||
+          n <= 0) {
+        (void)hipGetLastError();
+        n = 2;
+      }
+      occ = cached[dev][fp8 ? 1 : 0][d] = n;
+    }
+  }
+  return std::max(1, std::min(occ, by_lds));
+}
 
 struct Plan {
-  int P, stages, max_parts;
-  size_t ws_bytes;
+  int unit_tokens;   // tokens per unit (16 bf16, 32 fp8)
+  int min_chunk;     // minimum units per slice
+  int stages;
+  int grid;          // workgroups of the stream kernel
+  size_t dyn_lds;    // dynamic LDS bytes
+  size_t rec_o_off, rec_ml_off, plan_off, hdr_off, ws_bytes;
 };
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 int validate(const dp_decode_shape* sh, Plan* plan) {
   using dpool::fail;
@@ -513,6 +752,8 @@ int validate(const dp_decode_shape* sh, Plan* plan) {
     return fail(DP_ENOTSUP, "paged_decode: out_dtype %d", sh->out_dtype);
   if (sh->reserved != 0) return fail(DP_EINVAL, "paged_decode: reserved must be 0");
   if (sh->batch < 0 || sh->batch > 65535) return fail(DP_EINVAL, "paged_decode: batch %d outside [0, 65535]", sh->batch);
+  if (sh->batch > kMaxBatchInLds)
+    return fail(DP_ENOTSUP, "paged_decode: batch %d > %d sequences per call", sh->batch, kMaxBatchInLds);
   if (sh->n_q_heads <= 0 || sh->n_kv_heads <= 0 || sh->n_kv_heads > 65535 || sh->n_q_heads % sh->n_kv_heads)
     return fail(DP_EINVAL, "paged_decode: n_q_heads %d must be a positive multiple of n_kv_heads %d",
                 sh->n_q_heads, sh->n_kv_heads);
@@ -522,53 +763,60 @@ int validate(const dp_decode_shape* sh, Plan* plan) {
       (int64_t)sh->max_context_len > (int64_t)sh->max_blocks_per_seq * kBlock)
     return fail(DP_EINVAL, "paged_decode: max_context_len %d must be in [0, 16 * max_blocks_per_seq = %lld]",
                 sh->max_context_len, (long long)sh->max_blocks_per_seq * kBlock);
-  if (sh->num_blocks <= 0 || sh->num_blocks > (int64_t)INT32_MAX + 1)
-    return fail(DP_EINVAL, "paged_decode: num_blocks %lld", (long long)sh->num_blocks);
-  const int unit = sh->kv_dtype == DP_KV_FP8_E4M3 ? 32 : 16;
-  int P = sh->partition_tokens ? sh->partition_tokens : default_partition(sh);
-  if (P <= 0 || P % unit || P / kBlock > 64 * kWaves)
-    return fail(DP_EINVAL, "paged_decode: partition_tokens %d must be a positive multiple of %d and <= %d", P, unit,
-                64 * kWaves * kBlock);
-  int st = sh->pipeline_stages ? sh->pipeline_stages : default_stages(sh);
+  if (sh->num_blocks <= 0 || sh->num_blocks * (int64_t)sh->n_kv_heads > INT32_MAX)
+    return fail(DP_EINVAL, "paged_decode: num_blocks %lld (num_blocks * n_kv_heads must fit int32)",
+                (long long)sh->num_blocks);
+  const bool fp8 = sh->kv_dtype == DP_KV_FP8_E4M3;
+  const int unit = fp8 ? 32 : 16;
+  const int P = sh->partition_tokens;
+  if (P < 0 || P % unit || P / unit > kMaxUnitsPerWave)
+    return fail(DP_EINVAL, "paged_decode: partition_tokens %d must be a multiple of %d in [0, %d]", P, unit,
+                unit * kMaxUnitsPerWave);
+  const int st = sh->pipeline_stages ? sh->pipeline_stages : 3;
   if (st < 2 || st > 4) return fail(DP_EINVAL, "paged_decode: pipeline_stages %d outside [2, 4]", st);
-  plan->P = P;
+  const int64_t units_per_seq = ((int64_t)sh->max_context_len + unit - 1) / unit;
+  const int64_t max_units = units_per_seq * sh->batch * sh->n_kv_heads;
+  if (max_units > INT32_MAX) return fail(DP_ENOTSUP, "paged_decode: %lld units exceed int32", (long long)max_units);
+  plan->unit_tokens = unit;
+  plan->min_chunk = P ? P / unit : 8;
   plan->stages = st;
-  plan->max_parts = sh->max_context_len > 0 ? (sh->max_context_len + P - 1) / P : 1;
-  plan->ws_bytes = 0;
-  if (plan->max_parts > 1) {
-    const size_t rows = (size_t)sh->batch * sh->n_q_heads * plan->max_parts;
-    size_t o_bytes = rows * kHeadDim * sizeof(float);
-    o_bytes = (o_bytes + 255) & ~(size_t)255;
-    plan->ws_bytes = o_bytes + rows * 2 * sizeof(float);
-  }
+  // LDS per workgroup: V stages (4 KiB per unit) + tile indices + wave sums
+  // (static) + unit prefix and context lengths of the batch (dynamic)
+  const size_t stat = (size_t)kWaves * st * 4096 + (size_t)kWaves * kMaxUnitsPerWave * (fp8 ? 2 : 1) * 4 + 64;
+  plan->dyn_lds = (size_t)(2 * sh->batch + 1) * 4;
+  const size_t lds = stat + plan->dyn_lds;
+  if (lds > kLdsBytes) return fail(DP_ENOTSUP, "paged_decode: %zu bytes of LDS per workgroup", lds);
+  int dev = -1;
+  const int cus = device_cus(&dev);
+  const int per_cu = blocks_per_cu(dev, fp8, st - 1, lds);
+  // persistent grid: every workgroup resident at once, and no slice longer
+  // than kMaxUnitsPerWave
+  int64_t grid = (int64_t)cus * per_cu;
+  const int64_t need = (max_units + (int64_t)kWaves * kMaxUnitsPerWave - 1) / ((int64_t)kWaves * kMaxUnitsPerWave);
+  grid = std::max(grid, need);
+  const int64_t useful = (max_units + (int64_t)kWaves * plan->min_chunk - 1) / ((int64_t)kWaves * plan->min_chunk);
+  grid = std::max<int64_t>(1, std::min(grid, std::max(useful, need)));
+  plan->grid = (int)grid;
+  const int G = sh->n_q_heads / sh->n_kv_heads;
+  const size_t recs = (size_t)grid * kWaves * 2 * G;
+  plan->rec_o_off = 0;
+  plan->rec_ml_off = align256(recs * kHeadDim * sizeof(float));
+  plan->plan_off = plan->rec_ml_off + align256(recs * 2 * sizeof(float));
+  plan->hdr_off = plan->plan_off + align256((size_t)(sh->batch + 2) * sizeof(int32_t));
+  plan->ws_bytes = plan->hdr_off + align256((size_t)grid * kWaves * 4 * sizeof(int32_t));
   return DP_OK;
 }
 
 template <bool FP8, int ST>
-void launch_partition(dim3 grid, hipStream_t stream, const DecodeArgs& args) {
-  hipLaunchKernelGGL((paged_decode_partition_kernel<FP8, kWaves, ST>), grid, dim3(kWaves * 64), 0, stream, args);
+void launch_stream(const Plan& plan, hipStream_t stream, const StreamArgs& args) {
+  hipLaunchKernelGGL((paged_decode_stream_kernel<FP8, ST>), dim3(plan.grid), dim3(kWaves * 64), plan.dyn_lds,
+                     stream, args);
 }
-
-}  // namespace
-
-extern "C" size_t paged_decode_workspace_size(const dp_decode_shape* shape) {
-  Plan plan;
-  if (validate(shape, &plan) != DP_OK) return 0;
-  return plan.ws_bytes;
-}
-
-extern "C" int32_t paged_decode_partition_tokens(const dp_decode_shape* shape) {
-  Plan plan;
-  if (validate(shape, &plan) != DP_OK) return 0;
-  return plan.P;
-}
-
-namespace {
 
 // Validate everything the host can check and fill the kernel arguments.
 int prepare(const void* q, const void* k_blocks, const void* v_blocks, const int32_t* block_tables,
             const int32_t* context_lens, float scale, const float* k_scale, const float* v_scale, void* out,
-            const dp_decode_shape* shape, void* workspace, size_t workspace_bytes, Plan* plan, DecodeArgs* args) {
+            const dp_decode_shape* shape, void* workspace, size_t workspace_bytes, Plan* plan, StreamArgs* args) {
   using dpool::fail;
   int rc = validate(shape, plan);
   if (rc != DP_OK) return rc;
@@ -583,12 +831,10 @@ int prepare(const void* q, const void* k_blocks, const void* v_blocks, const int
   if (((uintptr_t)block_tables | (uintptr_t)context_lens) & 3)
     return fail(DP_EINVAL, "paged_decode: block_tables and context_lens must be 4-byte aligned");
   if (!std::isfinite(scale)) return fail(DP_EINVAL, "paged_decode: scale is not finite");
-  if (plan->ws_bytes > 0) {
-    if (!workspace || workspace_bytes < plan->ws_bytes)
-      return fail(DP_ENOMEM, "paged_decode: workspace needs %zu bytes, got %zu", plan->ws_bytes, workspace_bytes);
-    if ((uintptr_t)workspace & 255) return fail(DP_EINVAL, "paged_decode: workspace must be 256-byte aligned");
-  }
-  DecodeArgs& a = *args;
+  if (!workspace || workspace_bytes < plan->ws_bytes)
+    return fail(DP_ENOMEM, "paged_decode: workspace needs %zu bytes, got %zu", plan->ws_bytes, workspace_bytes);
+  if ((uintptr_t)workspace & 255) return fail(DP_EINVAL, "paged_decode: workspace must be 256-byte aligned");
+  StreamArgs& a = *args;
   a.q = (const uint16_t*)q;
   a.k = (const char*)k_blocks;
   a.v = (const char*)v_blocks;
@@ -597,14 +843,10 @@ int prepare(const void* q, const void* k_blocks, const void* v_blocks, const int
   a.k_scale = k_scale;
   a.v_scale = v_scale;
   a.out = out;
-  a.part_o = nullptr;
-  a.part_ml = nullptr;
-  if (plan->ws_bytes > 0) {
-    const size_t rows = (size_t)shape->batch * shape->n_q_heads * plan->max_parts;
-    const size_t o_bytes = (rows * kHeadDim * sizeof(float) + 255) & ~(size_t)255;
-    a.part_o = (float*)workspace;
-    a.part_ml = (float*)((char*)workspace + o_bytes);
-  }
+  a.rec_o = (float*)((char*)workspace + plan->rec_o_off);
+  a.rec_ml = (float*)((char*)workspace + plan->rec_ml_off);
+  a.plan = (int32_t*)((char*)workspace + plan->plan_off);
+  a.hdr = (int32_t*)((char*)workspace + plan->hdr_off);
   a.qk_scale_log2 = scale * kLog2e;
   a.batch = shape->batch;
   a.hq = shape->n_q_heads;
@@ -612,34 +854,31 @@ int prepare(const void* q, const void* k_blocks, const void* v_blocks, const int
   a.group = shape->n_q_heads / shape->n_kv_heads;
   a.max_blocks_per_seq = shape->max_blocks_per_seq;
   a.max_ctx = shape->max_context_len;
-  a.part_tokens = plan->P;
-  a.max_parts = plan->max_parts;
   a.num_blocks_m1 = (int32_t)(shape->num_blocks - 1);
   a.out_fp32 = shape->out_dtype == DP_OUT_FP32;
+  a.min_chunk = plan->min_chunk;
   return DP_OK;
 }
 
-int launch_partition_phase(const dp_decode_shape* shape, const Plan& plan, const DecodeArgs& args, hipStream_t st) {
-  const dim3 grid(plan.max_parts, shape->n_kv_heads, shape->batch);
+int launch_partition_phase(const dp_decode_shape* shape, const Plan& plan, const StreamArgs& args, hipStream_t st) {
   const bool fp8 = shape->kv_dtype == DP_KV_FP8_E4M3;
   (void)hipGetLastError();  // clear a stale error left by earlier work
-  switch (plan.stages * 2 + (fp8 ? 1 : 0)) {
-    case 4: launch_partition<false, 2>(grid, st, args); break;
-    case 5: launch_partition<true, 2>(grid, st, args); break;
-    case 6: launch_partition<false, 3>(grid, st, args); break;
-    case 7: launch_partition<true, 3>(grid, st, args); break;
-    case 8: launch_partition<false, 4>(grid, st, args); break;
-    default: launch_partition<true, 4>(grid, st, args); break;
+  switch ((plan.stages - 1) * 2 + (fp8 ? 1 : 0)) {
+    case 2: launch_stream<false, 1>(plan, st, args); break;
+    case 3: launch_stream<true, 1>(plan, st, args); break;
+    case 4: launch_stream<false, 2>(plan, st, args); break;
+    case 5: launch_stream<true, 2>(plan, st, args); break;
+    case 6: launch_stream<false, 3>(plan, st, args); break;
+    default: launch_stream<true, 3>(plan, st, args); break;
   }
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return dpool::fail(DP_EIO, "paged_decode: partition launch failed: %s", hipGetErrorString(e));
+  if (e != hipSuccess) return dpool::fail(DP_EIO, "paged_decode: stream kernel launch failed: %s", hipGetErrorString(e));
   return DP_OK;
 }
 
-int launch_merge_phase(const dp_decode_shape* shape, const Plan& plan, const DecodeArgs& args, hipStream_t st) {
-  if (plan.max_parts <= 1) return DP_OK;
+int launch_merge_phase(const Plan& plan, const StreamArgs& args, hipStream_t st) {
   (void)hipGetLastError();
-  hipLaunchKernelGGL(paged_decode_merge_kernel, dim3(shape->n_kv_heads, shape->batch), dim3(256), 0, st, args);
+  hipLaunchKernelGGL(paged_decode_merge_kernel, dim3(plan.grid * kWaves), dim3(256), 0, st, args);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return dpool::fail(DP_EIO, "paged_decode: merge launch failed: %s", hipGetErrorString(e));
   return DP_OK;
@@ -647,19 +886,31 @@ int launch_merge_phase(const dp_decode_shape* shape, const Plan& plan, const Dec
 
 }  // namespace
 
+extern "C" size_t paged_decode_workspace_size(const dp_decode_shape* shape) {
+  Plan plan;
+  if (validate(shape, &plan) != DP_OK) return 0;
+  return plan.ws_bytes;
+}
+
+extern "C" int32_t paged_decode_partition_tokens(const dp_decode_shape* shape) {
+  Plan plan;
+  if (validate(shape, &plan) != DP_OK) return 0;
+  return plan.min_chunk * plan.unit_tokens;
+}
+
 extern "C" int paged_decode_attention(const void* q, const void* k_blocks, const void* v_blocks,
                                       const int32_t* block_tables, const int32_t* context_lens, float scale,
                                       const float* k_scale, const float* v_scale, void* out,
                                       const dp_decode_shape* shape, void* workspace, size_t workspace_bytes,
                                       void* stream) {
   Plan plan;
-  DecodeArgs args;
+  StreamArgs args;
   int rc = prepare(q, k_blocks, v_blocks, block_tables, context_lens, scale, k_scale, v_scale, out, shape, workspace,
                    workspace_bytes, &plan, &args);
   if (rc != DP_OK || shape->batch == 0) return rc;
   rc = launch_partition_phase(shape, plan, args, (hipStream_t)stream);
   if (rc != DP_OK) return rc;
-  return launch_merge_phase(shape, plan, args, (hipStream_t)stream);
+  return launch_merge_phase(plan, args, (hipStream_t)stream);
 }
 
 extern "C" int paged_decode_partition(const void* q, const void* k_blocks, const void* v_blocks,
@@ -668,7 +919,7 @@ extern "C" int paged_decode_partition(const void* q, const void* k_blocks, const
                                       const dp_decode_shape* shape, void* workspace, size_t workspace_bytes,
                                       void* stream) {
   Plan plan;
-  DecodeArgs args;
+  StreamArgs args;
   int rc = prepare(q, k_blocks, v_blocks, block_tables, context_lens, scale, k_scale, v_scale, out, shape, workspace,
                    workspace_bytes, &plan, &args);
   if (rc != DP_OK || shape->batch == 0) return rc;
@@ -681,18 +932,18 @@ extern "C" int paged_decode_merge(const int32_t* context_lens, void* out, const 
   Plan plan;
   int rc = validate(shape, &plan);
   if (rc != DP_OK) return rc;
-  if (shape->batch == 0 || plan.max_parts <= 1) return DP_OK;
+  if (shape->batch == 0) return DP_OK;
   if (!context_lens || !out) return fail(DP_EINVAL, "paged_decode_merge: null tensor pointer");
   if (((uintptr_t)out & 15) || ((uintptr_t)context_lens & 3))
     return fail(DP_EINVAL, "paged_decode_merge: out must be 16-byte and context_lens 4-byte aligned");
   if (!workspace || workspace_bytes < plan.ws_bytes)
     return fail(DP_ENOMEM, "paged_decode_merge: workspace needs %zu bytes, got %zu", plan.ws_bytes, workspace_bytes);
   if ((uintptr_t)workspace & 255) return fail(DP_EINVAL, "paged_decode_merge: workspace must be 256-byte aligned");
-  DecodeArgs a = {};
-  const size_t rows = (size_t)shape->batch * shape->n_q_heads * plan.max_parts;
-  const size_t o_bytes = (rows * kHeadDim * sizeof(float) + 255) & ~(size_t)255;
-  a.part_o = (float*)workspace;
-  a.part_ml = (float*)((char*)workspace + o_bytes);
+  StreamArgs a = {};
+  a.rec_o = (float*)((char*)workspace + plan.rec_o_off);
+  a.rec_ml = (float*)((char*)workspace + plan.rec_ml_off);
+  a.plan = (int32_t*)((char*)workspace + plan.plan_off);
+  a.hdr = (int32_t*)((char*)workspace + plan.hdr_off);
   a.context_lens = context_lens;
   a.out = out;
   a.batch = shape->batch;
@@ -700,8 +951,7 @@ extern "C" int paged_decode_merge(const int32_t* context_lens, void* out, const 
   a.hkv = shape->n_kv_heads;
   a.group = shape->n_q_heads / shape->n_kv_heads;
   a.max_ctx = shape->max_context_len;
-  a.part_tokens = plan.P;
-  a.max_parts = plan.max_parts;
   a.out_fp32 = shape->out_dtype == DP_OUT_FP32;
-  return launch_merge_phase(shape, plan, a, (hipStream_t)stream);
+  a.min_chunk = plan.min_chunk;
+  return launch_merge_phase(plan, a, (hipStream_t)stream);
 }
