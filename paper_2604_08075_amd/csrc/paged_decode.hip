@@ -122,50 +122,50 @@ __device__ __forceinline__ bf16x8 fp8x8_to_bf16(int lo, int hi) {
   return r;
 }
 
-// LDS reads of the stage buffers, issued as inline asm: the compiler cannot
-// tell them apart from the in-flight direct-to-LDS loads into the other
-// stages and would wait for every outstanding global load first.  The caller
-// waits for completion with lds_wait_*(), which also carries the data
-// dependency into the consumers.
-__device__ __forceinline__ i32x2 ds_read_tr16(uint32_t lds_addr) {
-  i32x2 r;
-  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(r) : "v"(lds_addr) : "memory");
-  return r;
+// LDS reads of the V stages, issued as inline asm: through the builtins the
+// compiler cannot tell them apart from the direct-to-LDS loads in flight
+// into other stages and waits for every outstanding global load first.  Each
+// asm block issues its reads and waits for them (lgkmcnt(0)) before it ends,
+// so its outputs are complete when the compiler first sees them.
+__device__ __forceinline__ void ds_read_tr16_x8(uint32_t base, const int* off, i32x2 (&r)[8]) {
+  asm volatile(
+      "ds_read_b64_tr_b16 %0, %8\n\tds_read_b64_tr_b16 %1, %9\n\tds_read_b64_tr_b16 %2, %10\n\t"
+      "ds_read_b64_tr_b16 %3, %11\n\tds_read_b64_tr_b16 %4, %12\n\tds_read_b64_tr_b16 %5, %13\n\t"
+      "ds_read_b64_tr_b16 %6, %14\n\tds_read_b64_tr_b16 %7, %15\n\ts_waitcnt lgkmcnt(0)"
+      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]), "=&v"(r[7])
+      : "v"(base + off[0]), "v"(base + off[1]), "v"(base + off[2]), "v"(base + off[3]), "v"(base + off[4]),
+        "v"(base + off[5]), "v"(base + off[6]), "v"(base + off[7])
+      : "memory");
 }
-__device__ __forceinline__ i32x2 ds_read_tr8(uint32_t lds_addr) {
-  i32x2 r;
-  asm volatile("ds_read_b64_tr_b8 %0, %1" : "=v"(r) : "v"(lds_addr) : "memory");
-  return r;
-}
-__device__ __forceinline__ i32x4 ds_read_b128(uint32_t lds_addr) {
-  i32x4 r;
-  asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(lds_addr) : "memory");
-  return r;
-}
-__device__ __forceinline__ void lds_wait_4(i32x4 (&v)[4]) {
-  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]) : : "memory");
-}
-__device__ __forceinline__ void lds_wait_8(i32x2 (&v)[8]) {
-  asm volatile("s_waitcnt lgkmcnt(0)"
-               : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]), "+v"(v[7])
-               :
-               : "memory");
+__device__ __forceinline__ void ds_read_tr8_x8(uint32_t base, const int* off, i32x2 (&r)[8]) {
+  asm volatile(
+      "ds_read_b64_tr_b8 %0, %8\n\tds_read_b64_tr_b8 %1, %9\n\tds_read_b64_tr_b8 %2, %10\n\t"
+      "ds_read_b64_tr_b8 %3, %11\n\tds_read_b64_tr_b8 %4, %12\n\tds_read_b64_tr_b8 %5, %13\n\t"
+      "ds_read_b64_tr_b8 %6, %14\n\tds_read_b64_tr_b8 %7, %15\n\ts_waitcnt lgkmcnt(0)"
+      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]), "=&v"(r[7])
+      : "v"(base + off[0]), "v"(base + off[1]), "v"(base + off[2]), "v"(base + off[3]), "v"(base + off[4]),
+        "v"(base + off[5]), "v"(base + off[6]), "v"(base + off[7])
+      : "memory");
 }
 
-// A 16-byte global load the compiler does not track (so it adds no waits of
-// its own around the direct-to-LDS pipeline); vm_wait_all_4() waits for it.
-__device__ __forceinline__ i32x4 global_load_b128(const void* p) {
-  i32x4 r;
-  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(r) : "v"(p) : "memory");
-  return r;
+__device__ __forceinline__ void ds_read_b128_x4(uint32_t base, const int* off, i32x4 (&r)[4]) {
+  asm volatile(
+      "ds_read_b128 %0, %4\n\tds_read_b128 %1, %5\n\tds_read_b128 %2, %6\n\tds_read_b128 %3, %7\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3])
+      : "v"(base + off[0]), "v"(base + off[1]), "v"(base + off[2]), "v"(base + off[3])
+      : "memory");
 }
-__device__ __forceinline__ float global_load_f32(const float* p) {
-  float r;
-  asm volatile("global_load_dword %0, %1, off" : "=v"(r) : "v"(p) : "memory");
-  return r;
-}
-__device__ __forceinline__ void vm_wait_all_4(i32x4 (&v)[4], float& x, float& y) {
-  asm volatile("s_waitcnt vmcnt(0)" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(x), "+v"(y) : : "memory");
+// Four 16-byte global loads and a wait for them (vmcnt(0), which also drains
+// the wave's direct-to-LDS loads in flight) in one asm block.
+__device__ __forceinline__ void global_load_b128_x4_wait(const char* p0, const char* p1, const char* p2,
+                                                         const char* p3, i32x4 (&r)[4]) {
+  asm volatile(
+      "global_load_dwordx4 %0, %4, off\n\tglobal_load_dwordx4 %1, %5, off\n\t"
+      "global_load_dwordx4 %2, %6, off\n\tglobal_load_dwordx4 %3, %7, off\n\ts_waitcnt vmcnt(0)"
+      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3])
+      : "v"(p0), "v"(p1), "v"(p2), "v"(p3)
+      : "memory");
 }
 
 __device__ __forceinline__ uint16_t f32_to_bf16_bits(float x) {
@@ -187,69 +187,56 @@ __device__ __forceinline__ void vm_wait() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
-// Ties the K registers to the wait just issued, so no consumer moves above it.
-__device__ __forceinline__ void dep4(i32x4 (&k)[4]) {
-  asm volatile("" : "+v"(k[0]), "+v"(k[1]), "+v"(k[2]), "+v"(k[3]));
+// Wait for the direct-to-LDS loads of the unit being computed: `younger`
+// later units (LPU instructions each) are in flight, plus `extra` of this
+// unit's own loads issued after the ones waited for.
+template <int D, int LPU, int EXTRA>
+__device__ __forceinline__ void wait_unit(int younger) {
+  if (D >= 3 && younger >= 3) vm_wait<(D >= 3 ? EXTRA + 3 * LPU : 0)>();
+  else if (D >= 2 && younger == 2) vm_wait<(D >= 2 ? EXTRA + 2 * LPU : 0)>();
+  else if (younger == 1) vm_wait<EXTRA + LPU>();
+  else vm_wait<EXTRA>();
 }
 
-// Wait until the K registers of the unit being computed have landed, given
-// how many later units are already in flight (each unit issues its 4 K loads,
-// then its V loads).
-template <int D, int LPU, int VLD>
-__device__ __forceinline__ void wait_k(int younger, i32x4 (&k)[4]) {
-  if (D >= 3 && younger >= 3) vm_wait<(D >= 3 ? VLD + 3 * LPU : 0)>();
-  else if (D >= 2 && younger == 2) vm_wait<(D >= 2 ? VLD + 2 * LPU : 0)>();
-  else if (younger == 1) vm_wait<VLD + LPU>();
-  else vm_wait<VLD>();
-  dep4(k);
-}
-// Wait until the V tiles of the unit being computed are in LDS.
-template <int D, int LPU>
-__device__ __forceinline__ void wait_v(int younger) {
-  if (D >= 3 && younger >= 3) vm_wait<(D >= 3 ? 3 * LPU : 0)>();
-  else if (D >= 2 && younger == 2) vm_wait<(D >= 2 ? 2 * LPU : 0)>();
-  else if (younger == 1) vm_wait<LPU>();
-  else vm_wait<0>();
-}
-
-// Enqueue one unit: its K tile rows straight into this lane's registers in
-// the MFMA A-operand layout (4 x 16 bytes per lane), then its V tiles into an
-// LDS stage with direct-to-LDS loads (16 bytes per lane per instruction,
-// chunk-swizzled per row).  tiles[] holds the flat tile index
-// (block id * Hkv + head) of each block of each unit of the slice.
+// Enqueue the direct-to-LDS loads of one unit (its K tiles, then its V
+// tiles) into a stage.  Each lane moves 16 bytes per instruction; goff holds
+// its swizzled source offsets inside a tile; tiles[] holds the flat tile
+// index (block id * Hkv + head) of each block of each unit of the slice.
 template <bool FP8>
 __device__ __forceinline__ void issue_unit(const int* tiles, int ui, const char* kpool, const char* vpool,
-                                           const int* goff, const int* kgoff, int kblk, char* vst, i32x4 (&kr)[4]) {
+                                           const int* goff, char* st) {
   constexpr int UB = FP8 ? 2 : 1;
   constexpr int TILE = FP8 ? 2048 : 4096;
   constexpr int DMA_PER_TILE = TILE / 1024;
   int t[UB];
   for (int b = 0; b < UB; ++b) t[b] = __builtin_amdgcn_readfirstlane(tiles[ui * UB + b]);
-  const int tk = (FP8 && kblk) ? t[UB - 1] : t[0];
-  const char* kbase = kpool + (size_t)tk * TILE;
-  for (int c = 0; c < 4; ++c) kr[c] = global_load_b128(kbase + kgoff[c]);
+  for (int b = 0; b < UB; ++b) {
+    const char* kt = kpool + (size_t)t[b] * TILE;
+    for (int k = 0; k < DMA_PER_TILE; ++k)
+      __builtin_amdgcn_global_load_lds(kt + goff[k], (LDS_AS void*)(st + b * TILE + k * 1024), 16, 0, 0);
+  }
   for (int b = 0; b < UB; ++b) {
     const char* vt = vpool + (size_t)t[b] * TILE;
     for (int k = 0; k < DMA_PER_TILE; ++k)
-      __builtin_amdgcn_global_load_lds(vt + goff[k], (LDS_AS void*)(vst + b * TILE + k * 1024), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(vt + goff[k], (LDS_AS void*)(st + (UB + b) * TILE + k * 1024), 16, 0, 0);
   }
 }
 
-// D = units in flight ahead of the one being computed (1..3); the wave keeps
-// D + 1 register stages for K and D + 1 LDS stages for V.
+// D = units in flight ahead of the one being computed (1..3); each wave owns
+// D + 1 LDS stages of one unit's K and V tiles (8 KiB).
 template <bool FP8, int D>
 __global__ __launch_bounds__(kWaves * 64) void paged_decode_stream_kernel(StreamArgs a) {
   constexpr int NW = kWaves;
   constexpr int NS = D + 1;
   constexpr int UB = FP8 ? 2 : 1;                // blocks per unit
   constexpr int TILE = FP8 ? 2048 : 4096;        // bytes of one (block, head) tile
-  constexpr int VSTAGE = UB * TILE;              // V tiles of one unit
-  constexpr int VLD = UB * (TILE / 1024);        // V load instructions per unit
-  constexpr int LPU = 4 + VLD;                   // vector-memory instructions per unit
-  __shared__ __attribute__((aligned(1024))) char vstages[NW * NS * VSTAGE];
+  constexpr int STAGE = 2 * UB * TILE;           // K tiles then V tiles of one unit
+  constexpr int LPU = 2 * UB * (TILE / 1024);    // direct-to-LDS instructions per unit
+  constexpr int VLD = UB * (TILE / 1024);        // of which V
+  __shared__ __attribute__((aligned(1024))) char stages[NW * NS * STAGE];
   __shared__ int tiles_lds[NW][kMaxUnitsPerWave * UB];
   __shared__ int wave_sums[NW];
-  extern __shared__ int dyn[];                   // pre[B + 1] (unit prefix), ctxs[B]
+  extern __shared__ int dyn[];                   // pre[B + 1], ctxs[B], k_scale[Hkv], v_scale[Hkv]
 
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -258,10 +245,18 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_stream_kernel(Stream
   const int lj = lane >> 4;  // 16-lane row of the wave
   int* pre = dyn;
   int* ctxs = dyn + B + 1;
+  float* kscl = (float*)(dyn + 2 * B + 1);
+  float* vscl = kscl + Hkv;
 
   // ---- 1. prefix of units over sequences (every workgroup computes it) ----
   {
     const int T = NW * 64, tid = threadIdx.x;
+    if constexpr (FP8) {
+      for (int g = tid; g < Hkv; g += T) {
+        kscl[g] = a.k_scale[g];
+        vscl[g] = a.v_scale[g];
+      }
+    }
     const int per = (B + T - 1) / T;
     int local = 0;
     for (int k = 0; k < per; ++k) {
@@ -334,7 +329,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_stream_kernel(Stream
   }
 
   // ---- 3. per-lane offsets ----
-  int goff[TILE / 1024];  // V: source offset inside a tile for each direct-to-LDS instruction
+  int goff[TILE / 1024];  // source offset inside a tile for each direct-to-LDS instruction
   for (int k = 0; k < TILE / 1024; ++k) {
     if constexpr (FP8) {
       const int row = 8 * k + (lane >> 3);
@@ -344,31 +339,33 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_stream_kernel(Stream
       goff[k] = row * 256 + 16 * ((lane & 15) ^ swz_bf16(row));
     }
   }
-  int kgoff[4];   // K: bf16 chunk c -> row li, bytes 64c + 16lj ; fp8 (group q, half h) -> 2q + h
-  int kblk = 0;   // fp8: which block of the unit this lane's K rows come from
-  int voff[8];    // V: transposing-read offsets inside a V stage
+  int koff[4];  // K reads: bf16 chunk c ; fp8 (group q, half h) -> index 2q + h
+  int voff[8];  // V transposing reads
   if constexpr (FP8) {
-    kblk = li >> 3;
     for (int qg = 0; qg < 2; ++qg)
       for (int hh = 0; hh < 2; ++hh) {
         const int tau = 8 * (li >> 2) + 4 * qg + (li & 3);
-        kgoff[2 * qg + hh] = (tau & 15) * 128 + 16 * (4 * hh + lj);
+        const int b = tau >> 4, r = tau & 15;
+        koff[2 * qg + hh] = b * TILE + r * 128 + 16 * ((4 * hh + lj) ^ swz_fp8(r));
       }
     for (int nn = 0; nn < 8; ++nn) {
       const int tau = 8 * lj + (li >> 1);
       const int b = tau >> 4, r = tau & 15;
-      voff[nn] = b * TILE + r * 128 + 16 * (nn ^ swz_fp8(r)) + 8 * (lane & 1);
+      voff[nn] = UB * TILE + b * TILE + r * 128 + 16 * (nn ^ swz_fp8(r)) + 8 * (lane & 1);
     }
   } else {
-    for (int c = 0; c < 4; ++c) kgoff[c] = li * 256 + 16 * (4 * c + lj);
+    for (int c = 0; c < 4; ++c) koff[c] = li * 256 + 16 * ((4 * c + lj) ^ swz_bf16(li));
     for (int nn = 0; nn < 8; ++nn) {
       const int row = 4 * lj + (li >> 2);
-      voff[nn] = row * 256 + 16 * ((2 * nn + ((lane & 3) >> 1)) ^ swz_bf16(row)) + 8 * (lane & 1);
+      voff[nn] = TILE + row * 256 + 16 * ((2 * nn + ((lane & 3) >> 1)) ^ swz_bf16(row)) + 8 * (lane & 1);
     }
   }
+  int qoff[4];  // query reads: head li (padding heads re-read head 0 and are zeroed), chunk c
+  for (int c = 0; c < 4; ++c)
+    qoff[c] = ((li < G ? li : 0) * kHeadDim + (FP8 ? 64 * (c >> 1) + 16 * lj + 8 * (c & 1) : 32 * c + 8 * lj)) * 2;
 
   // ---- 4. walk the slice ----
-  char* const wv = vstages + w * NS * VSTAGE;
+  char* const wbase = stages + w * NS * STAGE;
   // compute-side position (uniform): segment (s, g), unit j inside it
   int cs_s, cs_g, cs_j, cs_nus;
   {
@@ -386,183 +383,165 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_stream_kernel(Stream
     // this wave terminates a split segment when its first piece continues a
     // segment begun by an earlier wave and the segment ends inside this slice
     const bool term = cs_j > 0 && cs_nus - cs_j <= n;
-    if (lane == 0)
-      *(i32x4*)(a.hdr + 4 * gw) = term ? i32x4{cs_s, cs_g, u0 - cs_j, cs_nus} : i32x4{0, 0, 0, 0};
+    if (lane == 0) *(i32x4*)(a.hdr + 4 * gw) = term ? i32x4{cs_s, cs_g, u0 - cs_j, cs_nus} : i32x4{0, 0, 0, 0};
   }
 
-  i32x4 kreg[NS][4];
-#pragma unroll
-  for (int S = 0; S < D; ++S)
-    if (S < n) issue_unit<FP8>(tiles, S, a.k, a.v, goff, kgoff, kblk, wv + S * VSTAGE, kreg[S]);
+  for (int ui = 0; ui < min(D, n); ++ui) issue_unit<FP8>(tiles, ui, a.k, a.v, goff, wbase + ui * STAGE);
 
-  bf16x8 qop[4];
+  i32x4 qcur[4];
   float m_run = -INFINITY, l_part = 0.f, cscale = 0.f, vsc = 1.0f;
   f32x4 acc[8];
   int piece_j0 = 0, ctx_s = 0;
   bool piece_first = true;
 
-  for (int base = 0; base < n; base += NS) {
-#pragma unroll
-    for (int S = 0; S < NS; ++S) {
-      const int ui = base + S;
-      if (ui >= n) break;
-      if (ui + D < n) {
-        __builtin_amdgcn_s_waitcnt((7 << 4) | (0 << 8) | (15) | (3 << 14));  // lgkmcnt(0): stage reads done
-        issue_unit<FP8>(tiles, ui + D, a.k, a.v, goff, kgoff, kblk, wv + ((S + D) % NS) * VSTAGE,
-                        kreg[(S + D) % NS]);
-      }
-      if (ui == 0 || cs_j == 0) {  // a new piece starts: its query group, fresh softmax state
-        piece_first = ui == 0;
-        piece_j0 = cs_j;
-        ctx_s = __builtin_amdgcn_readfirstlane(ctxs[cs_s]);
-        // lanes of padding heads (li >= G) load head g*G and are zeroed below
-        const uint16_t* qrow = a.q + ((size_t)cs_s * a.hq + cs_g * G + (li < G ? li : 0)) * kHeadDim;
-        i32x4 qraw[4];
-        for (int c = 0; c < 4; ++c)
-          qraw[c] = global_load_b128(qrow + (FP8 ? 64 * (c >> 1) + 16 * lj + 8 * (c & 1) : 32 * c + 8 * lj));
-        float ksc = 1.0f;
-        vsc = 1.0f;
-        if constexpr (FP8) {
-          ksc = global_load_f32(a.k_scale + cs_g);
-          vsc = global_load_f32(a.v_scale + cs_g);
-        }
-        vm_wait_all_4(qraw, ksc, vsc);  // drains this wave's loads in flight too (once per piece)
-        for (int c = 0; c < 4; ++c) {
-          if (li < G) {
-            qop[c] = __builtin_bit_cast(bf16x8, qraw[c]);
-          } else {
-            for (int e = 0; e < 8; ++e) qop[c][e] = (__bf16)0.f;
-          }
-        }
-        cscale = a.qk_scale_log2 * ksc;
-        m_run = -INFINITY;
-        l_part = 0.f;
-        for (int nn = 0; nn < 8; ++nn) acc[nn] = f32x4{0.f, 0.f, 0.f, 0.f};
-      }
-      const int younger = min(D, n - 1 - ui);
-      const uint32_t vst = (uint32_t)(uintptr_t)(const LDS_AS char*)(wv + S * VSTAGE);
-      const int unit_tok0 = cs_j * UB * kBlock;
-      const bool ragged = unit_tok0 + UB * kBlock > ctx_s;
-
-      wait_k<D, LPU, VLD>(younger, kreg[S]);  // K rows of this unit are in registers
-
-      constexpr int NZ = FP8 ? 8 : 4;  // scores per lane: bf16 tokens 4lj+r ; fp8 tokens 8lj+e
-      float z[NZ];
+  for (int ui = 0; ui < n; ++ui) {
+    if (ui + D < n) {
+      __builtin_amdgcn_s_waitcnt((7 << 4) | (0 << 8) | (15) | (3 << 14));  // lgkmcnt(0): stage reads done
+      issue_unit<FP8>(tiles, ui + D, a.k, a.v, goff, wbase + ((ui + D) % NS) * STAGE);
+    }
+    if (ui == 0 || cs_j == 0) {  // a new piece starts: its query group, fresh softmax state
+      piece_first = ui == 0;
+      piece_j0 = cs_j;
+      ctx_s = __builtin_amdgcn_readfirstlane(ctxs[cs_s]);
+      const char* qrow = (const char*)(a.q + ((size_t)cs_s * a.hq + cs_g * G) * kHeadDim);
+      global_load_b128_x4_wait(qrow + qoff[0], qrow + qoff[1], qrow + qoff[2], qrow + qoff[3], qcur);
+      if (li >= G)  // padding heads contribute zero scores
+        for (int c = 0; c < 4; ++c) qcur[c] = i32x4{0, 0, 0, 0};
+      float ksc = 1.0f;
       if constexpr (FP8) {
-        for (int qg = 0; qg < 2; ++qg) {
-          f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
-          for (int hh = 0; hh < 2; ++hh) {
-            const i32x4 raw = kreg[S][2 * qg + hh];
-            const bf16x8 k0 = fp8x8_to_bf16(raw[0], raw[1]);
-            const bf16x8 k1 = fp8x8_to_bf16(raw[2], raw[3]);
-            sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, qop[2 * hh], sacc, 0, 0, 0);
-            sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, qop[2 * hh + 1], sacc, 0, 0, 0);
-          }
-          for (int r = 0; r < 4; ++r) z[4 * qg + r] = sacc[r] * cscale;
+        ksc = kscl[cs_g];
+        vsc = vscl[cs_g];
+      }
+      cscale = a.qk_scale_log2 * ksc;
+      m_run = -INFINITY;
+      l_part = 0.f;
+      for (int nn = 0; nn < 8; ++nn) acc[nn] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    const int younger = min(D, n - 1 - ui);
+    const uint32_t st = (uint32_t)(uintptr_t)(const LDS_AS char*)(wbase + (ui % NS) * STAGE);
+    const int unit_tok0 = cs_j * UB * kBlock;
+    const bool ragged = unit_tok0 + UB * kBlock > ctx_s;
+
+    wait_unit<D, LPU, VLD>(younger);  // K tiles of this unit have landed
+    i32x4 kraw[4];
+    ds_read_b128_x4(st, koff, kraw);
+
+    constexpr int NZ = FP8 ? 8 : 4;  // scores per lane: bf16 tokens 4lj+r ; fp8 tokens 8lj+e
+    float z[NZ];
+    if constexpr (FP8) {
+      for (int qg = 0; qg < 2; ++qg) {
+        f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
+        for (int hh = 0; hh < 2; ++hh) {
+          const i32x4 raw = kraw[2 * qg + hh];
+          const bf16x8 k0 = fp8x8_to_bf16(raw[0], raw[1]);
+          const bf16x8 k1 = fp8x8_to_bf16(raw[2], raw[3]);
+          sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, __builtin_bit_cast(bf16x8, qcur[2 * hh]), sacc, 0, 0,
+                                                         0);
+          sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, __builtin_bit_cast(bf16x8, qcur[2 * hh + 1]), sacc, 0,
+                                                         0, 0);
         }
+        for (int r = 0; r < 4; ++r) z[4 * qg + r] = sacc[r] * cscale;
+      }
+      if (ragged)
+        for (int e = 0; e < 8; ++e)
+          if (unit_tok0 + 8 * lj + e >= ctx_s) z[e] = -INFINITY;
+    } else {
+      f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
+      for (int c = 0; c < 4; ++c)
+        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kraw[c]),
+                                                       __builtin_bit_cast(bf16x8, qcur[c]), sacc, 0, 0, 0);
+      for (int r = 0; r < 4; ++r) z[r] = sacc[r] * cscale;
+      if (ragged)
+        for (int r = 0; r < 4; ++r)
+          if (unit_tok0 + 4 * lj + r >= ctx_s) z[r] = -INFINITY;
+    }
+
+    // online softmax (base 2) for head li over this unit's tokens
+    float bmax = z[0];
+    for (int e = 1; e < NZ; ++e) bmax = fmaxf(bmax, z[e]);
+    bmax = xor_max(bmax);
+    const float m_new = fmaxf(m_run, bmax);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    __bf16 pb[NZ];
+    float psum = 0.f;
+    for (int e = 0; e < NZ; ++e) {
+      pb[e] = (__bf16)__builtin_amdgcn_exp2f(z[e] - m_new);
+      psum += (float)pb[e];
+    }
+    l_part = l_part * alpha + psum;
+    for (int nn = 0; nn < 8; ++nn) acc[nn] *= alpha;
+
+    wait_unit<D, LPU, 0>(younger);  // V tiles of this unit have landed
+
+    if constexpr (FP8) {
+      bf16x8 pop;
+      for (int e = 0; e < 8; ++e) pop[e] = pb[e];
+      i32x2 raw[8];
+      ds_read_tr8_x8(st, voff, raw);
+      for (int nn = 0; nn < 8; ++nn) {
+        bf16x8 vop = fp8x8_to_bf16(raw[nn][0], raw[nn][1]);
         if (ragged)
           for (int e = 0; e < 8; ++e)
-            if (unit_tok0 + 8 * lj + e >= ctx_s) z[e] = -INFINITY;
-      } else {
-        f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
-        for (int c = 0; c < 4; ++c)
-          sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kreg[S][c]), qop[c], sacc, 0, 0,
-                                                         0);
-        for (int r = 0; r < 4; ++r) z[r] = sacc[r] * cscale;
+            if (unit_tok0 + 8 * lj + e >= ctx_s) vop[e] = (__bf16)0.f;
+        acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop, acc[nn], 0, 0, 0);
+      }
+    } else {
+      bf16x4 pop;
+      for (int e = 0; e < 4; ++e) pop[e] = pb[e];
+      i32x2 raw[8];
+      ds_read_tr16_x8(st, voff, raw);
+      for (int nn = 0; nn < 8; ++nn) {
+        bf16x4 vop = __builtin_bit_cast(bf16x4, raw[nn]);
         if (ragged)
-          for (int r = 0; r < 4; ++r)
-            if (unit_tok0 + 4 * lj + r >= ctx_s) z[r] = -INFINITY;
+          for (int e = 0; e < 4; ++e)
+            if (unit_tok0 + 4 * lj + e >= ctx_s) vop[e] = (__bf16)0.f;
+        acc[nn] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vop, pop, acc[nn], 0, 0, 0);
       }
+    }
 
-      // online softmax (base 2) for head li over this unit's tokens
-      float bmax = z[0];
-      for (int e = 1; e < NZ; ++e) bmax = fmaxf(bmax, z[e]);
-      bmax = xor_max(bmax);
-      const float m_new = fmaxf(m_run, bmax);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
-      __bf16 pb[NZ];
-      float psum = 0.f;
-      for (int e = 0; e < NZ; ++e) {
-        pb[e] = (__bf16)__builtin_amdgcn_exp2f(z[e] - m_new);
-        psum += (float)pb[e];
-      }
-      l_part = l_part * alpha + psum;
-      for (int nn = 0; nn < 8; ++nn) acc[nn] *= alpha;
-
-      wait_v<D, LPU>(younger);  // V tiles of this unit are in LDS
-
-      if constexpr (FP8) {
-        bf16x8 pop;
-        for (int e = 0; e < 8; ++e) pop[e] = pb[e];
-        i32x2 raw[8];
-        for (int nn = 0; nn < 8; ++nn) raw[nn] = ds_read_tr8(vst + voff[nn]);
-        lds_wait_8(raw);
-        for (int nn = 0; nn < 8; ++nn) {
-          bf16x8 vop = fp8x8_to_bf16(raw[nn][0], raw[nn][1]);
-          if (ragged)
-            for (int e = 0; e < 8; ++e)
-              if (unit_tok0 + 8 * lj + e >= ctx_s) vop[e] = (__bf16)0.f;
-          acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop, acc[nn], 0, 0, 0);
-        }
-      } else {
-        bf16x4 pop;
-        for (int e = 0; e < 4; ++e) pop[e] = pb[e];
-        i32x2 raw[8];
-        for (int nn = 0; nn < 8; ++nn) raw[nn] = ds_read_tr16(vst + voff[nn]);
-        lds_wait_8(raw);
-        for (int nn = 0; nn < 8; ++nn) {
-          bf16x4 vop = __builtin_bit_cast(bf16x4, raw[nn]);
-          if (ragged)
-            for (int e = 0; e < 4; ++e)
-              if (unit_tok0 + 4 * lj + e >= ctx_s) vop[e] = (__bf16)0.f;
-          acc[nn] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vop, pop, acc[nn], 0, 0, 0);
-        }
-      }
-
-      // ---- end of a piece: write the result or a partial record ----
-      const bool seg_end = cs_j == cs_nus - 1;
-      if (seg_end || ui == n - 1) {
-        const float l_tot = xor_sum(l_part);
-        const float inv = vsc / l_tot;
-        if (li < G) {
-          if (piece_j0 == 0 && seg_end) {  // the whole segment: final output
-            const size_t row = ((size_t)cs_s * a.hq + cs_g * G + li) * kHeadDim;
-            for (int nn = 0; nn < 8; ++nn) {
-              const f32x4 o = acc[nn] * inv;
-              const size_t off = row + 16 * nn + 4 * lj;
-              if (a.out_fp32) {
-                *(f32x4*)((float*)a.out + off) = o;
-              } else {
-                u16x4 ob;
-                for (int e = 0; e < 4; ++e) ob[e] = f32_to_bf16_bits(o[e]);
-                *(u16x4*)((uint16_t*)a.out + off) = ob;
-              }
+    // ---- end of a piece: write the result or a partial record ----
+    const bool seg_end = cs_j == cs_nus - 1;
+    if (seg_end || ui == n - 1) {
+      const float l_tot = xor_sum(l_part);
+      const float inv = vsc / l_tot;
+      if (li < G) {
+        if (piece_j0 == 0 && seg_end) {  // the whole segment: final output
+          const size_t row = ((size_t)cs_s * a.hq + cs_g * G + li) * kHeadDim;
+          for (int nn = 0; nn < 8; ++nn) {
+            const f32x4 o = acc[nn] * inv;
+            const size_t off = row + 16 * nn + 4 * lj;
+            if (a.out_fp32) {
+              *(f32x4*)((float*)a.out + off) = o;
+            } else {
+              u16x4 ob;
+              for (int e = 0; e < 4; ++e) ob[e] = f32_to_bf16_bits(o[e]);
+              *(u16x4*)((uint16_t*)a.out + off) = ob;
             }
-          } else {  // a piece of a segment cut by slice boundaries
-            const size_t rec = (size_t)gw * 2 + (piece_first ? 0 : 1);
-            float* ro = a.rec_o + (rec * G + li) * kHeadDim;
-            for (int nn = 0; nn < 8; ++nn) *(f32x4*)(ro + 16 * nn + 4 * lj) = acc[nn] * inv;
-            if (lj == 0) {
-              a.rec_ml[(rec * G + li) * 2 + 0] = m_run;
-              a.rec_ml[(rec * G + li) * 2 + 1] = l_tot;
-            }
+          }
+        } else {  // a piece of a segment cut by slice boundaries
+          const size_t rec = (size_t)gw * 2 + (piece_first ? 0 : 1);
+          float* ro = a.rec_o + (rec * G + li) * kHeadDim;
+          for (int nn = 0; nn < 8; ++nn) *(f32x4*)(ro + 16 * nn + 4 * lj) = acc[nn] * inv;
+          if (lj == 0) {
+            a.rec_ml[(rec * G + li) * 2 + 0] = m_run;
+            a.rec_ml[(rec * G + li) * 2 + 1] = l_tot;
           }
         }
       }
-      // advance the compute-side position
-      if (ui + 1 < n) {
-        if (++cs_j == cs_nus) {
-          cs_j = 0;
-          if (++cs_g == Hkv) {
-            cs_g = 0;
-            do {
-              ++cs_s;
-            } while (cs_s < B - 1 && pre[cs_s + 1] == pre[cs_s]);  // skip empty sequences (bounded)
-            cs_s = __builtin_amdgcn_readfirstlane(cs_s);
-          }
-          cs_nus = __builtin_amdgcn_readfirstlane(pre[cs_s + 1] - pre[cs_s]);
+    }
+    // advance the compute-side position
+    if (ui + 1 < n) {
+      if (++cs_j == cs_nus) {
+        cs_j = 0;
+        if (++cs_g == Hkv) {
+          cs_g = 0;
+          do {
+            ++cs_s;
+          } while (cs_s < B - 1 && pre[cs_s + 1] == pre[cs_s]);  // skip empty sequences (bounded)
+          cs_s = __builtin_amdgcn_readfirstlane(cs_s);
         }
+        cs_nus = __builtin_amdgcn_readfirstlane(pre[cs_s + 1] - pre[cs_s]);
       }
     }
   }
@@ -605,17 +584,36 @@ __global__ __launch_bounds__(256) void paged_decode_merge_kernel(StreamArgs a) {
   float m_run = -INFINITY, l_run = 0.f;
   f32x4 acc[4] = {};
   if (grp < groups) {
-    for (int r = grp; r < nrec; r += groups) {
-      const size_t rec = r == 0 ? (size_t)first_slot : (size_t)(k0 + r) * 2;
-      const float* ml = a.rec_ml + (rec * G + i) * 2;
-      const float m = ml[0], l = ml[1];
-      const f32x4* o = (const f32x4*)(a.rec_o + (rec * G + i) * kHeadDim + d0);
-      const float m_new = fmaxf(m_run, m);
-      const float c_old = __builtin_amdgcn_exp2f(m_run - m_new);
-      const float c_new = l * __builtin_amdgcn_exp2f(m - m_new);
-      for (int e = 0; e < 4; ++e) acc[e] = acc[e] * c_old + o[e] * c_new;
-      l_run = l_run * c_old + c_new;
-      m_run = m_new;
+    constexpr int kBatch = 8;  // records whose loads are in flight together
+    for (int r0 = grp; r0 < nrec; r0 += groups * kBatch) {
+      float m[kBatch], l[kBatch];
+      f32x4 o[kBatch][4];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int r = r0 + u * groups;
+        if (r < nrec) {
+          const size_t rec = r == 0 ? (size_t)first_slot : (size_t)(k0 + r) * 2;
+          const float* ml = a.rec_ml + (rec * G + i) * 2;
+          m[u] = ml[0];
+          l[u] = ml[1];
+          const f32x4* op = (const f32x4*)(a.rec_o + (rec * G + i) * kHeadDim + d0);
+          for (int e = 0; e < 4; ++e) o[u][e] = op[e];
+        } else {
+          m[u] = -INFINITY;
+          l[u] = 0.f;
+          for (int e = 0; e < 4; ++e) o[u][e] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        if (m[u] == -INFINITY) continue;
+        const float m_new = fmaxf(m_run, m[u]);
+        const float c_old = __builtin_amdgcn_exp2f(m_run - m_new);
+        const float c_new = l[u] * __builtin_amdgcn_exp2f(m[u] - m_new);
+        for (int e = 0; e < 4; ++e) acc[e] = acc[e] * c_old + o[u][e] * c_new;
+        l_run = l_run * c_old + c_new;
+        m_run = m_new;
+      }
     }
   }
   __shared__ float sm[32][16], sl[32][16];
@@ -772,7 +770,7 @@ int validate(const dp_decode_shape* sh, Plan* plan) {
   if (P < 0 || P % unit || P / unit > kMaxUnitsPerWave)
     return fail(DP_EINVAL, "paged_decode: partition_tokens %d must be a multiple of %d in [0, %d]", P, unit,
                 unit * kMaxUnitsPerWave);
-  const int st = sh->pipeline_stages ? sh->pipeline_stages : 3;
+  const int st = sh->pipeline_stages ? sh->pipeline_stages : 2;
   if (st < 2 || st > 4) return fail(DP_EINVAL, "paged_decode: pipeline_stages %d outside [2, 4]", st);
   const int64_t units_per_seq = ((int64_t)sh->max_context_len + unit - 1) / unit;
   const int64_t max_units = units_per_seq * sh->batch * sh->n_kv_heads;
@@ -780,10 +778,10 @@ int validate(const dp_decode_shape* sh, Plan* plan) {
   plan->unit_tokens = unit;
   plan->min_chunk = P ? P / unit : 8;
   plan->stages = st;
-  // LDS per workgroup: V stages (4 KiB per unit) + tile indices + wave sums
-  // (static) + unit prefix and context lengths of the batch (dynamic)
-  const size_t stat = (size_t)kWaves * st * 4096 + (size_t)kWaves * kMaxUnitsPerWave * (fp8 ? 2 : 1) * 4 + 64;
-  plan->dyn_lds = (size_t)(2 * sh->batch + 1) * 4;
+  // LDS per workgroup: K+V stages (8 KiB per unit) + tile indices + wave sums
+  // (static) + unit prefix, context lengths and fp8 scales (dynamic)
+  const size_t stat = (size_t)kWaves * st * 8192 + (size_t)kWaves * kMaxUnitsPerWave * (fp8 ? 2 : 1) * 4 + 64;
+  plan->dyn_lds = (size_t)(2 * sh->batch + 1 + 2 * sh->n_kv_heads) * 4;
   const size_t lds = stat + plan->dyn_lds;
   if (lds > kLdsBytes) return fail(DP_ENOTSUP, "paged_decode: %zu bytes of LDS per workgroup", lds);
   int dev = -1;
