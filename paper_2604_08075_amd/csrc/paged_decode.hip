@@ -561,6 +561,10 @@ __global__ __launch_bounds__(256) void paged_decode_merge_kernel(StreamArgs a) {
   const int k = blockIdx.x;
   const int G = a.group, B = a.batch;
   const int tid = threadIdx.x;
+  // independent loads first: this wave's header, the slice length, and the
+  // prefix entries that say whether sequence k is empty
+  const i32x4 h = *(const i32x4*)(a.hdr + 4 * k);
+  const int C = a.plan[B + 1];
   for (int s = k; s < B; s += gridDim.x) {  // empty sequences: zero rows
     if (a.plan[s + 1] == a.plan[s]) {
       for (int idx = tid; idx < a.hq * 32; idx += 256) {
@@ -570,10 +574,8 @@ __global__ __launch_bounds__(256) void paged_decode_merge_kernel(StreamArgs a) {
       }
     }
   }
-  const i32x4 h = *(const i32x4*)(a.hdr + 4 * k);
   const int s = h[0], g = h[1], a0 = h[2], nus = h[3];
   if (nus == 0) return;  // wave k terminates no split segment
-  const int C = a.plan[B + 1];
   const int k0 = a0 / C;
   const int first_slot = k0 * 2 + (a0 > k0 * C ? 1 : 0);
   const int nrec = k - k0 + 1;
