@@ -1,10 +1,10 @@
 #!/usr/bin/env python3
 """Paged decode-attention benchmark on one MI355X.
 
-One "step" is one decode step of one layer for the whole batch: the
-partition kernel plus (when some sequence spans several partitions) the
-log-sum-exp merge kernel, i.e. every stage of the hot path, with the inputs
-already resident in HBM.  Successive steps rotate over R independent copies
+One "step" is one decode step of one layer for the whole batch: one launch
+of the decode kernel, which streams every cached K and V element once and
+merges split-K partials inside the same launch - every stage of the hot
+path, with the inputs already resident in HBM.  Successive steps rotate over R independent copies
 of the layer's KV pool (R * KV bytes >= 1 GiB), so the 256 MB Infinity
 Cache cannot serve a step from the previous one.
 
@@ -45,9 +45,9 @@ def kernel_sha() -> str:
 
 
 def measured_traffic(workload_name: str):
-    """HBM bytes per launch of the stream kernel from the committed rocprofv3
+    """HBM bytes per launch of the decode kernel from the committed rocprofv3
     counter summary, if it was taken on the kernel source as it is now."""
-    path = os.path.join(PROFILES, f"traffic_paged_decode_stream_{workload_name}.txt")
+    path = os.path.join(PROFILES, f"traffic_paged_decode_{workload_name}.txt")
     if not os.path.exists(path):
         return None
     vals = {}
@@ -69,7 +69,7 @@ def describe(w) -> str:
             f"sum ctx {int(w.context_lens.sum())}, max ctx {w.max_context_len}, pool {w.num_blocks} blocks")
 
 
-def measure(cfg: int, steps: int, warmup: int, partition_tokens: int, stages: int):
+def measure(cfg: int, steps: int, warmup: int, partition_tokens: int, wgs: int):
     import torch
 
     import workloads
@@ -83,7 +83,7 @@ def measure(cfg: int, steps: int, warmup: int, partition_tokens: int, stages: in
     fp8 = w.kv_format == "fp8_e4m3"
     dec = binding.PagedDecoder(w.batch, w.n_q_heads, w.n_kv_heads, w.max_blocks_per_seq, w.max_context_len,
                                w.num_blocks, kv_fp8=fp8, partition_tokens=partition_tokens,
-                               pipeline_stages=stages)
+                               workgroups_per_cu=wgs)
     out = dec.new_out()
     q, bt, cl, ks, vs = dev["q"], dev["block_tables"], dev["context_lens"], dev["k_scale"], dev["v_scale"]
     kl, vl = dev["k"], dev["v"]
@@ -104,27 +104,25 @@ def measure(cfg: int, steps: int, warmup: int, partition_tokens: int, stages: in
     torch.cuda.synchronize()
     ms_step = start.elapsed_time(end) / steps
 
-    # per-kernel durations: the same steps with events around each phase
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    # kernel duration: the same steps with events around each launch, on the
+    # launch stream (torch's current stream, which the binding passes down)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
     for i in range(steps):
         ev[i][0].record()
-        dec.partition(q, kl[i % layers], vl[i % layers], bt, cl, w.scale, out, ks, vs)
+        step(i)
         ev[i][1].record()
-        dec.merge(cl, out)
-        ev[i][2].record()
     torch.cuda.synchronize()
-    part_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / steps
-    merge_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / steps
+    kern_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / steps
     res = dict(
         workload=describe(w), name=w.name, batch=w.batch, kv_bytes=w.kv_bytes, kv_format=w.kv_format,
         ms_per_step=ms_step, gbs=w.kv_bytes / (ms_step * 1e-3) / 1e9,
-        seq_steps_per_s=w.batch / (ms_step * 1e-3), stream_kernel_ms=part_ms, merge_kernel_ms=merge_ms,
-        stream_kernel_gbs=w.kv_bytes / (part_ms * 1e-3) / 1e9, partition_tokens=dec.partition_tokens,
+        seq_steps_per_s=w.batch / (ms_step * 1e-3), kernel_ms=kern_ms,
+        kernel_gbs=w.kv_bytes / (kern_ms * 1e-3) / 1e9, partition_tokens=dec.partition_tokens,
         layers_rotated=layers, sum_ctx=int(w.context_lens.sum()),
         flops=4 * w.head_dim * w.n_q_heads * int(w.context_lens.sum()))
     log(f"config {cfg}: {ms_step * 1e3:.1f} us/step, {res['gbs']:.0f} GB/s "
-        f"({100 * res['gbs'] / PEAK_HBM_GBS:.1f}% of 8 TB/s), stream kernel {part_ms * 1e3:.1f} us, "
-        f"merge {merge_ms * 1e3:.1f} us, P={dec.partition_tokens}")
+        f"({100 * res['gbs'] / PEAK_HBM_GBS:.1f}% of 8 TB/s), kernel {kern_ms * 1e3:.1f} us "
+        f"({100 * res['kernel_gbs'] / PEAK_HBM_GBS:.1f}%), min slice {dec.partition_tokens} tokens")
     del dev
     torch.cuda.empty_cache()
     return res, w
@@ -168,7 +166,7 @@ def main():
     ap.add_argument("--long-config", type=int, default=3, help="long-pool workload reported beside it (0 = none)")
     ap.add_argument("--all", action="store_true", help="also report configs 1, 4 and 5")
     ap.add_argument("--partition-tokens", type=int, default=0)
-    ap.add_argument("--stages", type=int, default=0)
+    ap.add_argument("--wgs-per-cu", type=int, default=0, help="resident workgroups per CU (0 = library choice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB 10 times (counter calibration) and exit")
@@ -194,22 +192,22 @@ def main():
     from paper_2604_08075_amd import binding
     log(f"libdpool {binding.version()} on {torch.cuda.get_device_name(0)}")
 
-    head, w_head = measure(args.config, args.steps, args.warmup, args.partition_tokens, args.stages)
+    head, w_head = measure(args.config, args.steps, args.warmup, args.partition_tokens, args.wgs_per_cu)
     extra = {}
     if args.long_config:
-        r, _ = measure(args.long_config, args.steps, args.warmup, args.partition_tokens, args.stages)
+        r, _ = measure(args.long_config, args.steps, args.warmup, args.partition_tokens, args.wgs_per_cu)
         extra["long_pool"] = r
     if args.all:
         for c in (1, 4, 5):
             if c not in (args.config, args.long_config):
-                r, _ = measure(c, args.steps, args.warmup, args.partition_tokens, args.stages)
+                r, _ = measure(c, args.steps, args.warmup, args.partition_tokens, args.wgs_per_cu)
                 extra[f"config_{c}"] = r
 
     traffic = measured_traffic(head["name"])
-    roof = {"bound": "hbm", "achieved": head["stream_kernel_gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
-            "frac": head["stream_kernel_gbs"] / PEAK_HBM_GBS, "traffic": traffic,
-            "kernel": "paged_decode_stream_kernel", "algorithmic_bytes_per_launch": head["kv_bytes"],
-            "avg_launch_ms": head["stream_kernel_ms"]}
+    roof = {"bound": "hbm", "achieved": head["kernel_gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": head["kernel_gbs"] / PEAK_HBM_GBS, "traffic": traffic,
+            "kernel": "paged_decode_kernel", "algorithmic_bytes_per_launch": head["kv_bytes"],
+            "avg_launch_ms": head["kernel_ms"]}
     line = {
         "metric": METRIC, "value": head["gbs"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": head["ms_per_step"], "higher_is_better": True, "scaling": "weak",

@@ -159,24 +159,35 @@ int route_on_response(const dp_route_params* params, dp_cat_state* cats, int32_t
 /* PagedAttention blocks (Sec. 3 effect 3).  For sequence s with            */
 /* T = context_lens[s] and query head h (KV head g = h / G, G = Hq / Hkv):  */
 /*   K_t = k_scale[g] * k_blocks[block_tables[s][t/16], g, t%16, :]          */
-/*   V_t = v_scale[g] * v_blocks[block_tables[s][t/16], g, t%16, :]          */
+/*   V_t = v_scale[g] * v_blocks[block_tables[s][t/16], g, :, t%16]          */
 /*   out[s,h,:] = softmax_t(scale * q[s,h,:] . K_t) @ V                     */
 /* T = 0 gives a zero row.                                                   */
 /*                                                                           */
 /* Layouts (row-major, device memory, 16-byte aligned):                      */
 /*   q            [batch, n_q_heads, head_dim]            bf16               */
-/*   k_blocks,    [num_blocks, n_kv_heads, block_size, head_dim]             */
-/*   v_blocks       bf16 (DP_KV_BF16) or OCP e4m3 bytes (DP_KV_FP8_E4M3)     */
+/*   k_blocks     [num_blocks, n_kv_heads, block_size, head_dim]             */
+/*                (token-major: one token's dims are contiguous)             */
+/*   v_blocks     [num_blocks, n_kv_heads, head_dim, block_size]             */
+/*                (dims-major: one dim's 16 tokens are contiguous)           */
+/*                both bf16 (DP_KV_BF16) or OCP e4m3 bytes (DP_KV_FP8_E4M3); */
+/*                each (block, KV head) tile of K and of V is contiguous     */
 /*   block_tables [batch, max_blocks_per_seq] int32; entries past            */
-/*                ceil(T/16) are never read (may hold -1)                    */
+/*                ceil(T/16) are never read (may hold -1); ids outside       */
+/*                [0, num_blocks) are clamped into range, never dereferenced */
 /*   context_lens [batch] int32, each <= max_context_len (a caller promise;  */
-/*                larger values are clamped, never read out of bounds)      */
+/*                larger values are clamped, never read out of bounds).      */
+/*                Cache slots at t >= T of a sequence's last block are never */
+/*                used, whatever they hold                                   */
 /*   k_scale,     [n_kv_heads] fp32 per-head dequantisation scales (fp8      */
 /*   v_scale        only; must be NULL for bf16)                             */
 /*   out          [batch, n_q_heads, head_dim] bf16 (DP_OUT_BF16) or fp32    */
 /*   workspace    >= paged_decode_workspace_size(shape) bytes, 256-byte      */
-/*                aligned, caller-owned; may be NULL if that size is 0       */
-/* Supported: head_dim 128, block_size 16, 1 <= Hq/Hkv <= 16.                */
+/*                aligned, caller-owned.  It must be zero-filled before its  */
+/*                first use; every completed call leaves its arrival         */
+/*                counters at zero again, so one workspace serves any number */
+/*                of later calls, of any shape, in stream order.  Calls that */
+/*                share a workspace must not overlap in time.                */
+/* Supported: head_dim 128, block_size 16, 1 <= Hq/Hkv <= 16, batch <= 4096. */
 /* ------------------------------------------------------------------------ */
 #define DP_KV_BF16 0
 #define DP_KV_FP8_E4M3 1
@@ -191,56 +202,42 @@ typedef struct {
   int32_t block_size;
   int32_t max_blocks_per_seq;
   int32_t max_context_len;
-  int32_t kv_dtype;         /* DP_KV_*                                        */
-  int32_t out_dtype;        /* DP_OUT_*                                       */
-  int32_t partition_tokens; /* split-K partition length in tokens, a multiple  */
-                            /* of 16 (bf16) or 32 (fp8); 0 = library's choice */
-  int32_t pipeline_stages;  /* KV tiles in flight per wave, 2..4; 0 = choice  */
-  int32_t reserved;         /* must be 0                                      */
-  int64_t num_blocks;       /* blocks in k_blocks / v_blocks                   */
+  int32_t kv_dtype;          /* DP_KV_*                                       */
+  int32_t out_dtype;         /* DP_OUT_*                                      */
+  int32_t partition_tokens;  /* minimum tokens of KV one wave processes (the  */
+                             /* split-K granularity): a multiple of 32 (bf16) */
+                             /* or 64 (fp8); 0 = library's choice             */
+  int32_t workgroups_per_cu; /* resident workgroups per compute unit, 1..8    */
+                             /* (capped by occupancy); 0 = library's choice   */
+  int32_t reserved;          /* must be 0                                     */
+  int64_t num_blocks;        /* blocks in k_blocks / v_blocks                  */
 } dp_decode_shape;
 
-/* Bytes of workspace paged_decode_attention needs for this shape (0 when no
- * sequence can span more than one partition).  Returns 0 for invalid shapes. */
+/* Bytes of workspace paged_decode_attention needs for this shape (it depends
+ * on the device's compute-unit count and the GQA group).  Returns 0 for
+ * invalid shapes (the reason is in dp_last_error()). */
 size_t paged_decode_workspace_size(const dp_decode_shape* shape);
 
-/* The partition length (tokens) the library uses for this shape. */
+/* The minimum tokens per wave slice the library uses for this shape
+ * (0 for invalid shapes). */
 int32_t paged_decode_partition_tokens(const dp_decode_shape* shape);
 
-/* Launch the decode attention on `stream` (a hipStream_t; NULL = default
- * stream).  Validates the shape and pointer alignment on the host
- * (DP_EINVAL / DP_ENOTSUP / DP_ENOMEM for a short workspace), then enqueues
- * the partition phase and, when some sequence spans several partitions, the
- * merge phase (the two calls below, in that order).  DP_EIO if a launch
- * fails. */
+/* Enqueue the decode attention on `stream` (a hipStream_t; NULL = default
+ * stream) as one kernel launch.  Validates the shape and pointer alignment
+ * on the host (DP_EINVAL / DP_ENOTSUP; DP_ENOMEM for a short workspace;
+ * nothing is enqueued then); DP_EIO if the launch fails.
+ *
+ * Split-K over the context: the cached tokens of all (sequence, KV head)
+ * pairs are cut into equal slices, one per wave; a pair cut by slice
+ * boundaries leaves per-slice softmax partials (o_p, m_p, l_p) in the
+ * workspace, which the last slice to finish merges with log-sum-exp weights
+ * M = max_p m_p, w_p = l_p * 2^(m_p - M), out = sum_p w_p o_p / sum_p w_p.
+ * Results are deterministic: the same inputs and shape give the same bits. */
 int paged_decode_attention(const void* q, const void* k_blocks, const void* v_blocks,
                            const int32_t* block_tables, const int32_t* context_lens,
                            float scale, const float* k_scale, const float* v_scale,
                            void* out, const dp_decode_shape* shape, void* workspace,
                            size_t workspace_bytes, void* stream);
-
-/* Phase 1 alone (same arguments and checks as paged_decode_attention).
- * Splits every sequence into partitions of paged_decode_partition_tokens()
- * tokens (split-K over the context).  Rows of sequences that fit in one
- * partition are written to `out` directly; every other (sequence, head,
- * partition) leaves its softmax partial in the workspace:
- *   o_p [batch, n_q_heads, max_parts, 128] fp32, normalised by l_p,
- *   (m_p, l_p) [batch, n_q_heads, max_parts, 2] fp32, m_p in log2 units,
- * with max_parts = ceil(max_context_len / partition_tokens), o_p at offset 0
- * and (m_p, l_p) at the next 256-byte boundary.  A context-parallel caller
- * can exchange these partials between devices before phase 2. */
-int paged_decode_partition(const void* q, const void* k_blocks, const void* v_blocks,
-                           const int32_t* block_tables, const int32_t* context_lens,
-                           float scale, const float* k_scale, const float* v_scale,
-                           void* out, const dp_decode_shape* shape, void* workspace,
-                           size_t workspace_bytes, void* stream);
-
-/* Phase 2 alone: for every sequence that spans several partitions, merge its
- * partials with log-sum-exp weights, M = max_p m_p,
- * w_p = l_p * 2^(m_p - M), out = sum_p w_p o_p / sum_p w_p, and write `out`.
- * A no-op (DP_OK) when no sequence can span two partitions. */
-int paged_decode_merge(const int32_t* context_lens, void* out, const dp_decode_shape* shape,
-                       void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -18,12 +18,14 @@ with grouped-query heads and block-table indexing:
 
     blk_t = block_tables[s, t // bs],  slot_t = t % bs       (t = 0 .. T-1)
     K_t   = k_scale[g] * dec(k_blocks[blk_t, g, slot_t, :])
-    V_t   = v_scale[g] * dec(v_blocks[blk_t, g, slot_t, :])
+    V_t   = v_scale[g] * dec(v_blocks[blk_t, g, :, slot_t])
     z_t   = scale * sum_i dec(q[s, h, i]) * K_t[i]
     out[s, h, :] = sum_t exp(z_t - mu) V_t / sum_t exp(z_t - mu),  mu = max_t z_t
 
   dec() is the exact decode of the storage format (``numerics``); for bf16
-  storage k_scale = v_scale = 1.  Subtracting mu changes nothing
+  storage k_scale = v_scale = 1.  The tile layouts are the interface's (the
+  paper fixes none): a K tile is token-major [bs, D], a V tile dims-major
+  [D, bs].  Subtracting mu changes nothing
   mathematically; it only keeps exp() finite.  T = 0 gives a zero row
   (a reading: the paper never decodes an empty sequence).
 
@@ -45,11 +47,13 @@ import numpy as np
 from . import numerics
 
 
-def _gather_rows(pool, block_ids: np.ndarray, g: int, T: int, bs: int) -> np.ndarray:
+def _gather_rows(pool, block_ids: np.ndarray, g: int, T: int, bs: int, dims_major: bool) -> np.ndarray:
     """Raw storage codes of tokens 0..T-1 of one sequence for KV head g: [T, D]."""
     n_blocks = -(-T // bs)
-    tiles = pool[block_ids[:n_blocks]]            # [n_blocks, Hkv, bs, D]
-    rows = tiles[:, g].reshape(n_blocks * bs, -1)  # token-major
+    tiles = pool[block_ids[:n_blocks]][:, g]       # [n_blocks, bs, D] or [n_blocks, D, bs]
+    if dims_major:
+        tiles = tiles.transpose(0, 2, 1)
+    rows = tiles.reshape(n_blocks * bs, -1)        # token-major
     return rows[:T]
 
 
@@ -59,8 +63,9 @@ def paged_decode_attention(q_bits, k_pool, v_pool, block_tables, context_lens, s
     """float64 [B, Hq, D] attention output (rows not in ``seqs`` are left NaN).
 
     q_bits       : uint16 [B, Hq, D] bf16 codes of the new query token
-    k_pool/v_pool: indexable by an int array of block ids -> [n, Hkv, bs, D]
-                   storage codes (uint16 bf16 or uint8 e4m3)
+    k_pool       : indexable by an int array of block ids -> [n, Hkv, bs, D]
+    v_pool       : likewise -> [n, Hkv, D, bs]
+                   (storage codes: uint16 bf16 or uint8 e4m3)
     block_tables : int [B, max_blocks_per_seq]
     context_lens : int [B]
     k_scale/v_scale: float [Hkv] per-KV-head dequantization scales (fp8 only)
@@ -81,8 +86,8 @@ def paged_decode_attention(q_bits, k_pool, v_pool, block_tables, context_lens, s
             continue
         bt = np.asarray(block_tables[s])
         for g in range(Hkv):
-            K = ks[g] * numerics.decode(_gather_rows(k_pool, bt, g, T, block_size), kv_format)
-            V = vs[g] * numerics.decode(_gather_rows(v_pool, bt, g, T, block_size), kv_format)
+            K = ks[g] * numerics.decode(_gather_rows(k_pool, bt, g, T, block_size, False), kv_format)
+            V = vs[g] * numerics.decode(_gather_rows(v_pool, bt, g, T, block_size, True), kv_format)
             for h in range(g * G, (g + 1) * G):
                 z = scale * (K @ q[s, h])
                 w = np.exp(z - z.max())

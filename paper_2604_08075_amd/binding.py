@@ -30,7 +30,6 @@ EXPORTS = (
     "kv_pool_create", "kv_pool_info", "kv_pool_alloc_seq", "kv_pool_free_seq", "kv_pool_destroy",
     "route_default_params", "route_init", "route_requests", "route_on_response",
     "paged_decode_workspace_size", "paged_decode_partition_tokens", "paged_decode_attention",
-    "paged_decode_partition", "paged_decode_merge",
 )
 
 
@@ -65,7 +64,7 @@ class DecodeShape(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("block_size", ctypes.c_int32),
                 ("max_blocks_per_seq", ctypes.c_int32), ("max_context_len", ctypes.c_int32),
                 ("kv_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32),
-                ("partition_tokens", ctypes.c_int32), ("pipeline_stages", ctypes.c_int32),
+                ("partition_tokens", ctypes.c_int32), ("workgroups_per_cu", ctypes.c_int32),
                 ("reserved", ctypes.c_int32), ("num_blocks", ctypes.c_int64)]
 
 
@@ -101,9 +100,6 @@ def lib() -> ctypes.CDLL:
         L.paged_decode_partition_tokens.restype = ctypes.c_int32
         L.paged_decode_attention.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_float] + [ctypes.c_void_p] * 3 + [
             ctypes.POINTER(DecodeShape), ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
-        L.paged_decode_partition.argtypes = L.paged_decode_attention.argtypes
-        L.paged_decode_merge.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(DecodeShape),
-                                         ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
         _lib = L
     return _lib
 
@@ -220,10 +216,11 @@ def route_on_response(params, cats, cat: int, req_bytes: int, prompt_tokens: int
 # ---------------------------------------------------------------- decode
 
 def decode_shape(batch, n_q_heads, n_kv_heads, max_blocks_per_seq, max_context_len, num_blocks, kv_fp8=False,
-                 out_fp32=False, partition_tokens=0, pipeline_stages=0, head_dim=128, block_size=16) -> DecodeShape:
+                 out_fp32=False, partition_tokens=0, workgroups_per_cu=0, head_dim=128,
+                 block_size=16) -> DecodeShape:
     return DecodeShape(batch, n_q_heads, n_kv_heads, head_dim, block_size, max_blocks_per_seq, max_context_len,
                        KV_FP8_E4M3 if kv_fp8 else KV_BF16, OUT_FP32 if out_fp32 else OUT_BF16, partition_tokens,
-                       pipeline_stages, 0, num_blocks)
+                       workgroups_per_cu, 0, num_blocks)
 
 
 def workspace_size(shape: DecodeShape) -> int:
@@ -250,54 +247,37 @@ def _ws(workspace):
     return workspace.data_ptr(), workspace.numel() * workspace.element_size()
 
 
-def _decode_call(fn, q, k_blocks, v_blocks, block_tables, context_lens, scale, out, shape, workspace, k_scale,
-                 v_scale, stream):
-    ws_ptr, ws_bytes = _ws(workspace)
-    check(fn(q.data_ptr(), k_blocks.data_ptr(), v_blocks.data_ptr(), block_tables.data_ptr(),
-             context_lens.data_ptr(), float(scale), k_scale.data_ptr() if k_scale is not None else None,
-             v_scale.data_ptr() if v_scale is not None else None, out.data_ptr(), ctypes.byref(shape), ws_ptr,
-             ws_bytes, _stream_ptr(stream)))
-
-
 def paged_decode_attention(q, k_blocks, v_blocks, block_tables, context_lens, scale, out, shape: DecodeShape,
                            workspace=None, k_scale=None, v_scale=None, stream=None) -> None:
     """Enqueue the decode on `stream` (default: torch's current stream).  All tensors are
-    device tensors laid out as include/dpool.h documents; nothing is copied or converted."""
-    _decode_call(lib().paged_decode_attention, q, k_blocks, v_blocks, block_tables, context_lens, scale, out, shape,
-                 workspace, k_scale, v_scale, stream)
-
-
-def paged_decode_partition(q, k_blocks, v_blocks, block_tables, context_lens, scale, out, shape: DecodeShape,
-                           workspace=None, k_scale=None, v_scale=None, stream=None) -> None:
-    """Phase 1 only (partition kernel)."""
-    _decode_call(lib().paged_decode_partition, q, k_blocks, v_blocks, block_tables, context_lens, scale, out, shape,
-                 workspace, k_scale, v_scale, stream)
-
-
-def paged_decode_merge(context_lens, out, shape: DecodeShape, workspace=None, stream=None) -> None:
-    """Phase 2 only (log-sum-exp merge kernel)."""
+    device tensors laid out as include/dpool.h documents; nothing is copied or converted.
+    The workspace must have been zero-filled before its first use."""
     ws_ptr, ws_bytes = _ws(workspace)
-    check(lib().paged_decode_merge(context_lens.data_ptr(), out.data_ptr(), ctypes.byref(shape), ws_ptr, ws_bytes,
-                                   _stream_ptr(stream)))
+    check(lib().paged_decode_attention(
+        q.data_ptr(), k_blocks.data_ptr(), v_blocks.data_ptr(), block_tables.data_ptr(), context_lens.data_ptr(),
+        float(scale), k_scale.data_ptr() if k_scale is not None else None,
+        v_scale.data_ptr() if v_scale is not None else None, out.data_ptr(), ctypes.byref(shape), ws_ptr, ws_bytes,
+        _stream_ptr(stream)))
 
 
 class PagedDecoder:
     """Holds one decode shape and its workspace; calling it enqueues the decode.
 
     Device memory for the workspace comes from torch's allocator once, at
-    construction; each call only marshals pointers into paged_decode_attention.
+    construction, zero-filled as the library requires; each call only marshals
+    pointers into paged_decode_attention.
     """
 
     def __init__(self, batch, n_q_heads, n_kv_heads, max_blocks_per_seq, max_context_len, num_blocks,
-                 kv_fp8=False, out_fp32=False, partition_tokens=0, pipeline_stages=0, device="cuda"):
+                 kv_fp8=False, out_fp32=False, partition_tokens=0, workgroups_per_cu=0, device="cuda"):
         import torch
         self.shape = decode_shape(batch, n_q_heads, n_kv_heads, max_blocks_per_seq, max_context_len, num_blocks,
-                                  kv_fp8, out_fp32, partition_tokens, pipeline_stages)
+                                  kv_fp8, out_fp32, partition_tokens, workgroups_per_cu)
         self.partition_tokens = _partition_tokens(self.shape)
         if self.partition_tokens <= 0:
             raise DpoolError(DP_EINVAL, last_error())
         ws = workspace_size(self.shape)
-        self.workspace = torch.empty(ws, dtype=torch.uint8, device=device) if ws else None
+        self.workspace = torch.zeros(ws, dtype=torch.uint8, device=device) if ws else None
         self.out_dtype = torch.float32 if out_fp32 else torch.bfloat16
 
     def new_out(self, device="cuda"):
@@ -309,14 +289,4 @@ class PagedDecoder:
                  stream=None):
         paged_decode_attention(q, k_blocks, v_blocks, block_tables, context_lens, scale, out, self.shape,
                                self.workspace, k_scale, v_scale, stream)
-        return out
-
-    def partition(self, q, k_blocks, v_blocks, block_tables, context_lens, scale, out, k_scale=None, v_scale=None,
-                  stream=None):
-        paged_decode_partition(q, k_blocks, v_blocks, block_tables, context_lens, scale, out, self.shape,
-                               self.workspace, k_scale, v_scale, stream)
-        return out
-
-    def merge(self, context_lens, out, stream=None):
-        paged_decode_merge(context_lens, out, self.shape, self.workspace, stream)
         return out

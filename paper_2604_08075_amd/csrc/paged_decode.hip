@@ -7,40 +7,45 @@
 // effect 3).  Definition: for sequence s (T = context_lens[s] tokens) and
 // query head h with KV head g = h / G,
 //     out[s,h] = sum_t softmax_t(scale * q[s,h] . K_t) V_t,
-//     K_t / V_t = row t%16 of tile (block_tables[s][t/16], g), times the
-//     per-head fp8 scale when the cache is e4m3.
+//     K_t = k_blocks[block_tables[s][t/16], g, t%16, :]   (token-major tile)
+//     V_t = v_blocks[block_tables[s][t/16], g, :, t%16]   (dims-major tile)
+//     times the per-head fp8 scale when the cache is e4m3.
 //
 // Work decomposition (stream-K over the KV stream).  The cached tokens of
-// every (sequence, KV head) "segment" form one flat stream of units (a unit
-// is one 16-token block for bf16, two for fp8), segments in sequence-major,
-// head-minor order.  A persistent grid sized to the device gives every wave
-// one contiguous, equal-length slice of that stream, so the load is balanced
-// to one unit however skewed the context lengths are, and no workgroup is
-// launched without work.  A wave walks its slice across segment boundaries
-// without draining its load pipeline.  A segment that lies wholly inside one
-// slice is finished in registers and written to `out`; a segment cut by slice
-// boundaries leaves one softmax partial per piece (each wave has at most two
-// such pieces: its first and its last), merged afterwards with log-sum-exp
-// weights by the merge kernel.
+// every (sequence, KV head) "segment" form one flat stream of 16 KiB units
+// (two 16-token blocks for bf16, four for fp8), segments in sequence-major,
+// head-minor order.  A persistent grid gives every wave one contiguous,
+// equal-length slice of that stream, so the load is balanced to one unit
+// however skewed the context lengths are.  A wave walks its slice across
+// segment boundaries without draining its load pipeline.  A segment that
+// lies wholly inside one slice is finished in registers and written to
+// `out`; a segment cut by slice boundaries leaves one softmax partial per
+// piece (a wave has at most two such pieces: its first and its last).  At the
+// end of its slice a wave signals its pieces on per-segment arrival counters;
+// the wave that brings a segment's last piece merges the partials with
+// log-sum-exp weights, reading them in a fixed order (deterministic).
 //
-// Per wave, the hot loop:
-//   * gfx950's direct-to-LDS loads (global_load_lds_dwordx4, 16 B per lane)
-//     move each unit's K and V tiles into one of NSTAGE private LDS stages,
-//     so NSTAGE-1 units stay in flight at no VGPR cost; a (block, head) tile
-//     is one contiguous 4 KiB (bf16) / 2 KiB (fp8) region read exactly once;
-//   * S^T = K Q^T on MFMA (v_mfma_f32_16x16x32_bf16: 16 tokens x 16 query
-//     heads, heads past the GQA group are zero padding), so every query head
-//     of the group reuses the tile from LDS;
-//   * the score accumulator layout is exactly the B operand of O^T = V^T P,
-//     so probabilities never move between lanes; V^T comes out of LDS
-//     through the transposing reads ds_read_b64_tr_b16 / _b8;
+// Per wave, the hot loop keeps one unit in flight while it computes the
+// previous one, with every byte going straight to registers in the layout
+// the matrix cores consume (no LDS staging):
+//   * K: one 16-byte load per lane per (32-dim chunk, 16-token row group)
+//     puts a token row's dims directly into the A operand of
+//     v_mfma_f32_16x16x32_bf16; S^T = K Q^T gives 16 tokens x 16 query heads
+//     (heads past the GQA group are zero padding), so every query head of
+//     the group reuses the tile.  The tokens behind the MFMA rows are
+//     permuted so that each lane's score accumulators are exactly the
+//     tokens its PV operand needs: probabilities never move between lanes;
+//   * V: the dims-major tile gives each lane 8 consecutive tokens of one
+//     head dimension per 16-byte load: the A operand of O^T = V^T P^T;
 //   * online softmax in base 2 (scale * log2 e folded into one multiply),
-//     the per-head max crossing the four 16-lane rows by two swizzles; O^T
-//     keeps each head in one lane column, so the running-max rescale is
-//     lane-local;
+//     the per-head max crossing the four 16-lane rows by two lane swaps;
+//     the running-max rescale is skipped when no head's max grew;
 //   * fp8 e4m3 tiles widen to bf16 exactly (v_cvt_scalef32_pk_bf16_fp8 with
 //     scale 1); the per-head K scale folds into the score multiplier, the V
 //     scale into the final normalisation.
+// Blocks past a sequence's last token are never loaded; tail slots of its
+// last block are masked by select (scores to -inf, values to 0), so poisoned
+// or stale cache contents cannot leak into the result.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -55,34 +60,30 @@
 namespace dpool_hip {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef int i32x2 __attribute__((ext_vector_type(2)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
-
-#define LDS_AS __attribute__((address_space(3)))
+typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kHeadDim = 128;
 constexpr int kBlock = 16;
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kWaves = 4;                 // waves per workgroup
-constexpr int kMaxUnitsPerWave = 256;     // the host sizes the grid so that no slice is longer
+constexpr int kWaves = 4;              // waves per workgroup
+constexpr int kMaxUnitsPerWave = 256;  // the host sizes the grid so that no slice is longer
 
-struct StreamArgs {
+struct DecodeArgs {
   const uint16_t* q;            // [B, Hq, 128] bf16
   const char* k;                // [num_blocks, Hkv, 16, 128] bf16 or e4m3
-  const char* v;
+  const char* v;                // [num_blocks, Hkv, 128, 16] bf16 or e4m3
   const int32_t* block_tables;  // [B, max_blocks_per_seq]
   const int32_t* context_lens;  // [B]
   const float* k_scale;         // [Hkv] (fp8)
   const float* v_scale;
   void* out;                    // [B, Hq, 128] bf16 or fp32
-  float* rec_o;                 // [waves, 2, G, 128]  partial outputs (normalised)
-  float* rec_ml;                // [waves, 2, G, 2]    (max in log2 units, sum)
-  int32_t* plan;                // [B + 2]: unit prefix over sequences, then the slice length
-  int32_t* hdr;                 // [waves, 4]: (s, g, a0, nus) of the segment a wave terminates, nus = 0 if none
+  int32_t* arrivals;            // [2, waves]: group and segment arrival counters; zero between calls
+  float* rec_ml;                // [3 * waves, G, 2]    (max in log2 units, sum)
+  float* rec_o;                 // [3 * waves, G, 128]  partial outputs (normalised, V-scaled)
   float qk_scale_log2;          // scale * log2(e)
   int32_t batch, hq, hkv, group;
   int32_t max_blocks_per_seq, max_ctx;
@@ -91,15 +92,20 @@ struct StreamArgs {
   int32_t min_chunk;            // minimum units per slice
 };
 
-// ----- LDS swizzles: 16-byte chunk permutations per row, chosen so that the
-// MFMA-layout reads (16 rows, same logical chunk) and the transposing reads
-// (4 or 8 rows, adjacent chunks) hit distinct banks.
-__device__ __forceinline__ int swz_bf16(int row) {  // 16 chunks per 256-byte row
-  return ((row & 3) << 1) | ((row >> 2) & 1) | (row & 8);
-}
-__device__ __forceinline__ int swz_fp8(int row) {  // 8 chunks per 128-byte row
-  return (row & 3) | ((((row >> 2) ^ (row >> 3)) & 1) << 2);
-}
+// Unit geometry: a unit is 16 KiB of K and V of one KV head.
+template <bool FP8>
+struct Geo {
+  static constexpr int UB = FP8 ? 4 : 2;          // blocks per unit
+  static constexpr int UT = UB * kBlock;          // tokens per unit
+  static constexpr int TILE = FP8 ? 2048 : 4096;  // bytes of one (block, head) tile
+  static constexpr int NZ = FP8 ? 16 : 8;         // scores per lane per unit
+};
+
+// One unit in registers: eight 16-byte K fragments and eight V fragments per lane.
+struct UnitRegs {
+  i32x4 k[8];
+  i32x4 v[8];
+};
 
 __device__ __forceinline__ float xor_max(float x) {
   x = fmaxf(x, __shfl_xor(x, 16));
@@ -122,127 +128,164 @@ __device__ __forceinline__ bf16x8 fp8x8_to_bf16(int lo, int hi) {
   return r;
 }
 
-// LDS reads of the V stages, issued as inline asm: through the builtins the
-// compiler cannot tell them apart from the direct-to-LDS loads in flight
-// into other stages and waits for every outstanding global load first.  Each
-// asm block issues its reads and waits for them (lgkmcnt(0)) before it ends,
-// so its outputs are complete when the compiler first sees them.
-__device__ __forceinline__ void ds_read_tr16_x8(uint32_t base, const int* off, i32x2 (&r)[8]) {
-  asm volatile(
-      "ds_read_b64_tr_b16 %0, %8\n\tds_read_b64_tr_b16 %1, %9\n\tds_read_b64_tr_b16 %2, %10\n\t"
-      "ds_read_b64_tr_b16 %3, %11\n\tds_read_b64_tr_b16 %4, %12\n\tds_read_b64_tr_b16 %5, %13\n\t"
-      "ds_read_b64_tr_b16 %6, %14\n\tds_read_b64_tr_b16 %7, %15\n\ts_waitcnt lgkmcnt(0)"
-      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]), "=&v"(r[7])
-      : "v"(base + off[0]), "v"(base + off[1]), "v"(base + off[2]), "v"(base + off[3]), "v"(base + off[4]),
-        "v"(base + off[5]), "v"(base + off[6]), "v"(base + off[7])
-      : "memory");
-}
-__device__ __forceinline__ void ds_read_tr8_x8(uint32_t base, const int* off, i32x2 (&r)[8]) {
-  asm volatile(
-      "ds_read_b64_tr_b8 %0, %8\n\tds_read_b64_tr_b8 %1, %9\n\tds_read_b64_tr_b8 %2, %10\n\t"
-      "ds_read_b64_tr_b8 %3, %11\n\tds_read_b64_tr_b8 %4, %12\n\tds_read_b64_tr_b8 %5, %13\n\t"
-      "ds_read_b64_tr_b8 %6, %14\n\tds_read_b64_tr_b8 %7, %15\n\ts_waitcnt lgkmcnt(0)"
-      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3]), "=&v"(r[4]), "=&v"(r[5]), "=&v"(r[6]), "=&v"(r[7])
-      : "v"(base + off[0]), "v"(base + off[1]), "v"(base + off[2]), "v"(base + off[3]), "v"(base + off[4]),
-        "v"(base + off[5]), "v"(base + off[6]), "v"(base + off[7])
-      : "memory");
+// Zero the elements at positions >= nv (0..8) of eight bf16.
+__device__ __forceinline__ bf16x8 keep_first(bf16x8 x, int nv) {
+  for (int e = 0; e < 8; ++e)
+    if (e >= nv) x[e] = (__bf16)0.f;
+  return x;
 }
 
-__device__ __forceinline__ void ds_read_b128_x4(uint32_t base, const int* off, i32x4 (&r)[4]) {
-  asm volatile(
-      "ds_read_b128 %0, %4\n\tds_read_b128 %1, %5\n\tds_read_b128 %2, %6\n\tds_read_b128 %3, %7\n\t"
-      "s_waitcnt lgkmcnt(0)"
-      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3])
-      : "v"(base + off[0]), "v"(base + off[1]), "v"(base + off[2]), "v"(base + off[3])
-      : "memory");
-}
-// Four 16-byte global loads and a wait for them (vmcnt(0), which also drains
-// the wave's direct-to-LDS loads in flight) in one asm block.
-__device__ __forceinline__ void global_load_b128_x4_wait(const char* p0, const char* p1, const char* p2,
-                                                         const char* p3, i32x4 (&r)[4]) {
-  asm volatile(
-      "global_load_dwordx4 %0, %4, off\n\tglobal_load_dwordx4 %1, %5, off\n\t"
-      "global_load_dwordx4 %2, %6, off\n\tglobal_load_dwordx4 %3, %7, off\n\ts_waitcnt vmcnt(0)"
-      : "=&v"(r[0]), "=&v"(r[1]), "=&v"(r[2]), "=&v"(r[3])
-      : "v"(p0), "v"(p1), "v"(p2), "v"(p3)
-      : "memory");
-}
-
-__device__ __forceinline__ uint16_t f32_to_bf16_bits(float x) {
-  return __builtin_bit_cast(uint16_t, (__bf16)x);
-}
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
 
 __device__ __forceinline__ int clamp_ctx(int c, int max_ctx) { return c < 0 ? 0 : (c > max_ctx ? max_ctx : c); }
 
 template <bool FP8>
 __device__ __forceinline__ int units_of(int ctx) {
-  const int nb = (ctx + kBlock - 1) / kBlock;
-  return FP8 ? (nb + 1) >> 1 : nb;
+  return (ctx + Geo<FP8>::UT - 1) / Geo<FP8>::UT;
 }
 
-template <int N>
-__device__ __forceinline__ void vm_wait() {
-  // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
-  // vmcnt[3:0] | expcnt[6:4]=7 | lgkmcnt[11:8]=15 | vmcnt[5:4] in [15:14]).
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+// Partial records cross compute units on different XCDs, whose L2 caches are
+// not coherent with each other.  They are written and read with agent-scope
+// atomic accesses (sc1: written through to, and read from, the coherence
+// point), so no L2-wide writeback or invalidate is needed: those stall every
+// wave streaming through the same L2.
+__device__ __forceinline__ void coherent_store4(float* p, f32x4 v) {
+  typedef unsigned long long u64;
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  __hip_atomic_store((u64*)p, __builtin_bit_cast(u64, f32x2{v[0], v[1]}), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store((u64*)p + 1, __builtin_bit_cast(u64, f32x2{v[2], v[3]}), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
 }
-// Wait for the direct-to-LDS loads of the unit being computed: `younger`
-// later units (LPU instructions each) are in flight, plus `extra` of this
-// unit's own loads issued after the ones waited for.
-template <int D, int LPU, int EXTRA>
-__device__ __forceinline__ void wait_unit(int younger) {
-  if (D >= 3 && younger >= 3) vm_wait<(D >= 3 ? EXTRA + 3 * LPU : 0)>();
-  else if (D >= 2 && younger == 2) vm_wait<(D >= 2 ? EXTRA + 2 * LPU : 0)>();
-  else if (younger == 1) vm_wait<EXTRA + LPU>();
-  else vm_wait<EXTRA>();
+__device__ __forceinline__ void coherent_store2(float* p, float a, float b) {
+  typedef unsigned long long u64;
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  __hip_atomic_store((u64*)p, __builtin_bit_cast(u64, f32x2{a, b}), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ f32x4 coherent_load4(const float* p) {
+  typedef unsigned long long u64;
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  const f32x2 lo = __builtin_bit_cast(f32x2, __hip_atomic_load((u64*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+  const f32x2 hi =
+      __builtin_bit_cast(f32x2, __hip_atomic_load((u64*)p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+  return f32x4{lo[0], lo[1], hi[0], hi[1]};
+}
+__device__ __forceinline__ void coherent_load2(const float* p, float& a, float& b) {
+  typedef unsigned long long u64;
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  const f32x2 v = __builtin_bit_cast(f32x2, __hip_atomic_load((u64*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+  a = v[0];
+  b = v[1];
 }
 
-// Enqueue the direct-to-LDS loads of one unit (its K tiles, then its V
-// tiles) into a stage.  Each lane moves 16 bytes per instruction; goff holds
-// its swizzled source offsets inside a tile; tiles[] holds the flat tile
-// index (block id * Hkv + head) of each block of each unit of the slice.
+// Write 8 consecutive output values (fp32 or bf16) of one row.
+__device__ __forceinline__ void store_out8(const DecodeArgs& a, size_t off, f32x4 x0, f32x4 x1) {
+  if (a.out_fp32) {
+    *(f32x4*)((float*)a.out + off) = x0;
+    *(f32x4*)((float*)a.out + off + 4) = x1;
+  } else {
+    u16x8 o;
+    for (int e = 0; e < 4; ++e) {
+      o[e] = f32_to_bf16_bits(x0[e]);
+      o[4 + e] = f32_to_bf16_bits(x1[e]);
+    }
+    *(u16x8*)((uint16_t*)a.out + off) = o;
+  }
+}
+
+// Record slots: 2k and 2k + 1 hold the first and last split piece of wave k;
+// 2 * waves + k holds the merged record of the group of pieces whose last
+// piece is wave k's.  A record is (o, m, l): o normalised by l, m in log2
+// units.  Pieces are merged in groups of kFanIn consecutive pieces, then the
+// group records, so that no merge folds more than kFanIn records per memory
+// round trip on each level (a long segment can be cut into many pieces).
+constexpr int kFanIn = 8;
+
+// Log-sum-exp fold of n records, by one wave, in record order:
+// M = max_p m_p, w_p = l_p 2^(m_p - M), o = sum_p w_p o_p / sum_p w_p,
+// L = sum_p w_p.  The result goes to the output rows of segment (s, g), or
+// to record slot dst.  slot_of(i) names the i-th record's slot.
+template <class SlotOf>
+__device__ __forceinline__ void merge_records(const DecodeArgs& a, SlotOf slot_of, int n, bool to_out, int s, int g,
+                                              size_t dst, int lane) {
+  const int G = a.group;
+  const int npairs = G * 16;  // (head, 8-value chunk) pairs
+  for (int p0 = 0; p0 < npairs; p0 += 128) {  // two pairs per lane at a time
+    int hd[2], d0[2];
+    bool ok[2];
+    for (int i = 0; i < 2; ++i) {
+      const int p = p0 + lane + 64 * i;
+      ok[i] = p < npairs;
+      const int pp = ok[i] ? p : 0;  // idle lanes re-read pair 0 and discard it
+      hd[i] = pp >> 4;
+      d0[i] = (pp & 15) * 8;
+    }
+    float M[2] = {-INFINITY, -INFINITY}, L[2] = {0.f, 0.f};
+    f32x4 o0[2] = {}, o1[2] = {};
+    for (int r0 = 0; r0 < n; r0 += kFanIn) {
+      float m[kFanIn][2], l[kFanIn][2];
+      f32x4 x0[kFanIn][2], x1[kFanIn][2];
+#pragma unroll
+      for (int u = 0; u < kFanIn; ++u) {
+        if (r0 + u < n) {
+          const size_t slot = slot_of(r0 + u);
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            coherent_load2(a.rec_ml + (slot * G + hd[i]) * 2, m[u][i], l[u][i]);
+            const float* ro = a.rec_o + (slot * G + hd[i]) * kHeadDim + d0[i];
+            x0[u][i] = coherent_load4(ro);
+            x1[u][i] = coherent_load4(ro + 4);
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kFanIn; ++u) {
+        if (r0 + u < n) {
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            const float M2 = fmaxf(M[i], m[u][i]);
+            const float c_old = __builtin_amdgcn_exp2f(M[i] - M2);
+            const float c_new = l[u][i] * __builtin_amdgcn_exp2f(m[u][i] - M2);
+            o0[i] = o0[i] * c_old + x0[u][i] * c_new;
+            o1[i] = o1[i] * c_old + x1[u][i] * c_new;
+            L[i] = L[i] * c_old + c_new;
+            M[i] = M2;
+          }
+        }
+      }
+    }
+    for (int i = 0; i < 2; ++i) {
+      if (!ok[i]) continue;
+      const float inv = 1.0f / L[i];
+      if (to_out) {
+        store_out8(a, ((size_t)s * a.hq + (size_t)g * G + hd[i]) * kHeadDim + d0[i], o0[i] * inv, o1[i] * inv);
+      } else {
+        float* ro = a.rec_o + (dst * G + hd[i]) * kHeadDim + d0[i];
+        coherent_store4(ro, o0[i] * inv);
+        coherent_store4(ro + 4, o1[i] * inv);
+        if (d0[i] == 0) coherent_store2(a.rec_ml + (dst * G + hd[i]) * 2, M[i], L[i]);
+      }
+    }
+  }
+}
+
+// Per-wave walker over the flat unit stream: segment (s, g), unit j inside it.
+struct Walker {
+  int s, g, j, nus;
+};
+
 template <bool FP8>
-__device__ __forceinline__ void issue_unit(const int* tiles, int ui, const char* kpool, const char* vpool,
-                                           const int* goff, char* st) {
-  constexpr int UB = FP8 ? 2 : 1;
-  constexpr int TILE = FP8 ? 2048 : 4096;
-  constexpr int DMA_PER_TILE = TILE / 1024;
-  int t[UB];
-  for (int b = 0; b < UB; ++b) t[b] = __builtin_amdgcn_readfirstlane(tiles[ui * UB + b]);
-  for (int b = 0; b < UB; ++b) {
-    const char* kt = kpool + (size_t)t[b] * TILE;
-    for (int k = 0; k < DMA_PER_TILE; ++k)
-      __builtin_amdgcn_global_load_lds(kt + goff[k], (LDS_AS void*)(st + b * TILE + k * 1024), 16, 0, 0);
-  }
-  for (int b = 0; b < UB; ++b) {
-    const char* vt = vpool + (size_t)t[b] * TILE;
-    for (int k = 0; k < DMA_PER_TILE; ++k)
-      __builtin_amdgcn_global_load_lds(vt + goff[k], (LDS_AS void*)(st + (UB + b) * TILE + k * 1024), 16, 0, 0);
-  }
-}
-
-// D = units in flight ahead of the one being computed (1..3); each wave owns
-// D + 1 LDS stages of one unit's K and V tiles (8 KiB).
-template <bool FP8, int D>
-__global__ __launch_bounds__(kWaves * 64) void paged_decode_stream_kernel(StreamArgs a) {
-  constexpr int NW = kWaves;
-  constexpr int NS = D + 1;
-  constexpr int UB = FP8 ? 2 : 1;                // blocks per unit
-  constexpr int TILE = FP8 ? 2048 : 4096;        // bytes of one (block, head) tile
-  constexpr int STAGE = 2 * UB * TILE;           // K tiles then V tiles of one unit
-  constexpr int LPU = 2 * UB * (TILE / 1024);    // direct-to-LDS instructions per unit
-  constexpr int VLD = UB * (TILE / 1024);        // of which V
-  __shared__ __attribute__((aligned(1024))) char stages[NW * NS * STAGE];
-  __shared__ int tiles_lds[NW][kMaxUnitsPerWave * UB];
-  __shared__ int wave_sums[NW];
-  extern __shared__ int dyn[];                   // pre[B + 1], ctxs[B], k_scale[Hkv], v_scale[Hkv]
+__global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a) {
+  using GE = Geo<FP8>;
+  constexpr int UB = GE::UB, UT = GE::UT, TILE = GE::TILE, NZ = GE::NZ;
+  __shared__ int tiles_lds[kWaves][kMaxUnitsPerWave * UB];
+  __shared__ int wave_sums[kWaves];
+  extern __shared__ int dyn[];  // pre[B + 1], ctxs[B], k_scale[Hkv], v_scale[Hkv]
 
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int B = a.batch, Hkv = a.hkv, G = a.group;
-  const int li = lane & 15;  // MFMA column (head) / row index
-  const int lj = lane >> 4;  // 16-lane row of the wave
+  const int li = lane & 15;  // MFMA row / column index
+  const int lj = lane >> 4;  // k-group (16-lane row of the wave)
   int* pre = dyn;
   int* ctxs = dyn + B + 1;
   float* kscl = (float*)(dyn + 2 * B + 1);
@@ -250,11 +293,11 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_stream_kernel(Stream
 
   // ---- 1. prefix of units over sequences (every workgroup computes it) ----
   {
-    const int T = NW * 64, tid = threadIdx.x;
+    const int T = kWaves * 64, tid = threadIdx.x;
     if constexpr (FP8) {
-      for (int g = tid; g < Hkv; g += T) {
-        kscl[g] = a.k_scale[g];
-        vscl[g] = a.v_scale[g];
+      for (int i = tid; i < Hkv; i += T) {
+        kscl[i] = a.k_scale[i];
+        vscl[i] = a.v_scale[i];
       }
     }
     const int per = (B + T - 1) / T;
@@ -287,23 +330,26 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_stream_kernel(Stream
     __syncthreads();
   }
   const int U = Hkv * pre[B];
-  const int TW = gridDim.x * NW;
+  const int TW = gridDim.x * kWaves;
   int C = (U + TW - 1) / TW;
   if (C < a.min_chunk) C = a.min_chunk;
-  if (blockIdx.x == 0) {  // the merge kernel needs the prefix and the slice length
-    for (int s = threadIdx.x; s <= B; s += NW * 64) a.plan[s] = pre[s];
-    if (threadIdx.x == 0) a.plan[B + 1] = C;
+  const int gw = blockIdx.x * kWaves + w;
+
+  // rows of empty sequences are zero
+  for (int s = gw; s < B; s += TW) {
+    if (ctxs[s] == 0) {
+      const size_t row0 = (size_t)s * a.hq * kHeadDim;
+      for (int e = lane * 8; e < a.hq * kHeadDim; e += 64 * 8)
+        store_out8(a, row0 + e, f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f});
+    }
   }
-  const int gw = blockIdx.x * NW + w;
+
   const int u0 = gw * C;
   const int u1 = min(u0 + C, U);
-  if (u0 >= u1) {  // no work: no segment to terminate
-    if (lane == 0) *(i32x4*)(a.hdr + 4 * gw) = i32x4{0, 0, 0, 0};
-    return;  // no barrier follows: waves are independent from here on
-  }
+  if (u0 >= u1) return;  // no work; no barrier follows: waves are independent from here on
   const int n = u1 - u0;
 
-  // ---- 2. tile indices of this wave's units into LDS ----
+  // ---- 2. tile indices (block id * Hkv + head) of this wave's units ----
   int* tiles = tiles_lds[w];
   for (int i = lane; i < n; i += 64) {
     const int u = u0 + i;
@@ -320,54 +366,45 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_stream_kernel(Stream
     const int j = r - g * nus;
     const int nb = (ctxs[s] + kBlock - 1) / kBlock;
     for (int b = 0; b < UB; ++b) {
-      int blk = j * UB + b;
-      if (blk >= nb) blk = j * UB;  // absent second block of an fp8 unit: reload the first (masked later)
+      // a block past the sequence's end is never fetched: its lanes re-read the
+      // unit's first block (same addresses as other lanes of the same load
+      // instruction, so no extra memory traffic) and its tokens are masked
+      const int blk = j * UB + (j * UB + b < nb ? b : 0);
       int id = a.block_tables[(size_t)s * a.max_blocks_per_seq + blk];
       id = id < 0 ? 0 : (id > a.num_blocks_m1 ? a.num_blocks_m1 : id);
       tiles[i * UB + b] = id * Hkv + g;
     }
   }
 
-  // ---- 3. per-lane offsets ----
-  int goff[TILE / 1024];  // source offset inside a tile for each direct-to-LDS instruction
-  for (int k = 0; k < TILE / 1024; ++k) {
-    if constexpr (FP8) {
-      const int row = 8 * k + (lane >> 3);
-      goff[k] = row * 128 + 16 * ((lane & 7) ^ swz_fp8(row));
-    } else {
-      const int row = 4 * k + (lane >> 4);
-      goff[k] = row * 256 + 16 * ((lane & 15) ^ swz_bf16(row));
-    }
-  }
-  int koff[4];  // K reads: bf16 chunk c ; fp8 (group q, half h) -> index 2q + h
-  int voff[8];  // V transposing reads
+  // ---- 3. per-lane operand offsets inside a tile ----
+  int kofs[8], vofs[8];
+  int kblk, vblk;  // which block of the unit this lane's K / V fragments come from
   if constexpr (FP8) {
-    for (int qg = 0; qg < 2; ++qg)
-      for (int hh = 0; hh < 2; ++hh) {
-        const int tau = 8 * (li >> 2) + 4 * qg + (li & 3);
-        const int b = tau >> 4, r = tau & 15;
-        koff[2 * qg + hh] = b * TILE + r * 128 + 16 * ((4 * hh + lj) ^ swz_fp8(r));
-      }
-    for (int nn = 0; nn < 8; ++nn) {
-      const int tau = 8 * lj + (li >> 1);
-      const int b = tau >> 4, r = tau & 15;
-      voff[nn] = UB * TILE + b * TILE + r * 128 + 16 * (nn ^ swz_fp8(r)) + 8 * (lane & 1);
-    }
+    // K: MFMA m (0..3), row li = token 4m + (li & 3) of block li >> 2; fragment j = dims 64j + 16lj .. +16
+    for (int m = 0; m < 4; ++m)
+      for (int jj = 0; jj < 2; ++jj) kofs[2 * m + jj] = (4 * m + (li & 3)) * 128 + 64 * jj + 16 * lj;
+    kblk = li >> 2;
+    // V: dim 16nn + li, all 16 tokens of block lj
+    for (int nn = 0; nn < 8; ++nn) vofs[nn] = (16 * nn + li) * 16;
+    vblk = lj;
   } else {
-    for (int c = 0; c < 4; ++c) koff[c] = li * 256 + 16 * ((4 * c + lj) ^ swz_bf16(li));
-    for (int nn = 0; nn < 8; ++nn) {
-      const int row = 4 * lj + (li >> 2);
-      voff[nn] = TILE + row * 256 + 16 * ((2 * nn + ((lane & 3) >> 1)) ^ swz_bf16(row)) + 8 * (lane & 1);
-    }
+    // K: MFMA m (0..1), row li = token 8((li >> 2) & 1) + 4m + (li & 3) of block li >> 3; chunk c = dims 32c + 8lj
+    for (int m = 0; m < 2; ++m)
+      for (int c = 0; c < 4; ++c) kofs[4 * m + c] = (8 * ((li >> 2) & 1) + 4 * m + (li & 3)) * 256 + 64 * c + 16 * lj;
+    kblk = li >> 3;
+    // V: dim 16nn + li, tokens 8(lj & 1) .. +8 of block lj >> 1
+    for (int nn = 0; nn < 8; ++nn) vofs[nn] = (16 * nn + li) * 32 + 16 * (lj & 1);
+    vblk = lj >> 1;
   }
-  int qoff[4];  // query reads: head li (padding heads re-read head 0 and are zeroed), chunk c
-  for (int c = 0; c < 4; ++c)
-    qoff[c] = ((li < G ? li : 0) * kHeadDim + (FP8 ? 64 * (c >> 1) + 16 * lj + 8 * (c & 1) : 32 * c + 8 * lj)) * 2;
+  // query fragment c of head li: the dims its K fragment holds.  Columns past
+  // the GQA group repeat a real head; they only ever affect their own
+  // (unwritten) output columns.
+  int qoff[4];
+  for (int c = 0; c < 4; ++c) qoff[c] = FP8 ? 64 * (c >> 1) + 16 * lj + 8 * (c & 1) : 32 * c + 8 * lj;
+  const int qhead = li < G ? li : li % G;
 
   // ---- 4. walk the slice ----
-  char* const wbase = stages + w * NS * STAGE;
-  // compute-side position (uniform): segment (s, g), unit j inside it
-  int cs_s, cs_g, cs_j, cs_nus;
+  Walker cs;  // compute side
   {
     int lo = 0, hi = B - 1;
     while (lo < hi) {
@@ -375,291 +412,267 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_stream_kernel(Stream
       if (Hkv * pre[mid] <= u0) lo = mid;
       else hi = mid - 1;
     }
-    cs_s = __builtin_amdgcn_readfirstlane(lo);
-    cs_nus = __builtin_amdgcn_readfirstlane(pre[cs_s + 1] - pre[cs_s]);
-    const int r = u0 - Hkv * pre[cs_s];
-    cs_g = __builtin_amdgcn_readfirstlane(r / cs_nus);
-    cs_j = __builtin_amdgcn_readfirstlane(r - cs_g * cs_nus);
-    // this wave terminates a split segment when its first piece continues a
-    // segment begun by an earlier wave and the segment ends inside this slice
-    const bool term = cs_j > 0 && cs_nus - cs_j <= n;
-    if (lane == 0) *(i32x4*)(a.hdr + 4 * gw) = term ? i32x4{cs_s, cs_g, u0 - cs_j, cs_nus} : i32x4{0, 0, 0, 0};
+    cs.s = __builtin_amdgcn_readfirstlane(lo);
+    cs.nus = __builtin_amdgcn_readfirstlane(pre[cs.s + 1] - pre[cs.s]);
+    const int r = u0 - Hkv * pre[cs.s];
+    cs.g = __builtin_amdgcn_readfirstlane(r / cs.nus);
+    cs.j = __builtin_amdgcn_readfirstlane(r - cs.g * cs.nus);
   }
+  auto advance = [&](Walker& wk) {
+    if (++wk.j == wk.nus) {
+      wk.j = 0;
+      if (++wk.g == Hkv) {
+        wk.g = 0;
+        do {
+          ++wk.s;
+        } while (wk.s < B - 1 && pre[wk.s + 1] == pre[wk.s]);  // skip empty sequences (bounded)
+        wk.s = __builtin_amdgcn_readfirstlane(wk.s);
+      }
+      wk.nus = __builtin_amdgcn_readfirstlane(pre[wk.s + 1] - pre[wk.s]);
+    }
+  };
+  // Every load below is unconditional, so the compiler's wait counts stay
+  // exact: a wait for one unit never drains the unit behind it.
+  auto load_q = [&](i32x4 (&qr)[4], int s, int g) {
+    const uint16_t* qrow = a.q + ((size_t)s * a.hq + (size_t)g * G + qhead) * kHeadDim;
+    for (int c = 0; c < 4; ++c) qr[c] = *(const i32x4*)(qrow + qoff[c]);
+  };
+  auto issue = [&](UnitRegs& R, int ui) {
+    const char* kb = a.k + (size_t)tiles[ui * UB + kblk] * TILE;
+    const char* vb = a.v + (size_t)tiles[ui * UB + vblk] * TILE;
+#pragma unroll
+    for (int x = 0; x < 8; ++x) R.k[x] = __builtin_nontemporal_load((const i32x4*)(kb + kofs[x]));
+#pragma unroll
+    for (int x = 0; x < 8; ++x) R.v[x] = __builtin_nontemporal_load((const i32x4*)(vb + vofs[x]));
+  };
 
-  for (int ui = 0; ui < min(D, n); ++ui) issue_unit<FP8>(tiles, ui, a.k, a.v, goff, wbase + ui * STAGE);
-
-  i32x4 qcur[4];
+  i32x4 qv[4];  // query group of the piece being computed; reloaded right after a segment's last unit
   float m_run = -INFINITY, l_part = 0.f, cscale = 0.f, vsc = 1.0f;
   f32x4 acc[8];
+  for (int nn = 0; nn < 8; ++nn) acc[nn] = f32x4{0.f, 0.f, 0.f, 0.f};
   int piece_j0 = 0, ctx_s = 0;
   bool piece_first = true;
+  // split segments this wave must signal: (s, g) of its first piece and of its last piece, s = -1 if none
+  int arr_s0 = -1, arr_g0 = 0, arr_s1 = -1, arr_g1 = 0;
 
-  for (int ui = 0; ui < n; ++ui) {
-    if (ui + D < n) {
-      __builtin_amdgcn_s_waitcnt((7 << 4) | (0 << 8) | (15) | (3 << 14));  // lgkmcnt(0): stage reads done
-      issue_unit<FP8>(tiles, ui + D, a.k, a.v, goff, wbase + ((ui + D) % NS) * STAGE);
-    }
-    if (ui == 0 || cs_j == 0) {  // a new piece starts: its query group, fresh softmax state
+  auto begin_piece = [&](int ui) {
+    if (ui == 0 || cs.j == 0) {  // a new piece starts: its query group, fresh softmax state
       piece_first = ui == 0;
-      piece_j0 = cs_j;
-      ctx_s = __builtin_amdgcn_readfirstlane(ctxs[cs_s]);
-      const char* qrow = (const char*)(a.q + ((size_t)cs_s * a.hq + cs_g * G) * kHeadDim);
-      global_load_b128_x4_wait(qrow + qoff[0], qrow + qoff[1], qrow + qoff[2], qrow + qoff[3], qcur);
-      if (li >= G)  // padding heads contribute zero scores
-        for (int c = 0; c < 4; ++c) qcur[c] = i32x4{0, 0, 0, 0};
+      piece_j0 = cs.j;
+      ctx_s = __builtin_amdgcn_readfirstlane(ctxs[cs.s]);
       float ksc = 1.0f;
       if constexpr (FP8) {
-        ksc = kscl[cs_g];
-        vsc = vscl[cs_g];
+        ksc = kscl[cs.g];
+        vsc = vscl[cs.g];
       }
       cscale = a.qk_scale_log2 * ksc;
       m_run = -INFINITY;
       l_part = 0.f;
       for (int nn = 0; nn < 8; ++nn) acc[nn] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    const int younger = min(D, n - 1 - ui);
-    const uint32_t st = (uint32_t)(uintptr_t)(const LDS_AS char*)(wbase + (ui % NS) * STAGE);
-    const int unit_tok0 = cs_j * UB * kBlock;
-    const bool ragged = unit_tok0 + UB * kBlock > ctx_s;
+  };
 
-    wait_unit<D, LPU, VLD>(younger);  // K tiles of this unit have landed
-    i32x4 kraw[4];
-    ds_read_b128_x4(st, koff, kraw);
+  auto compute_unit = [&](const UnitRegs& R) {
+    const int unit_tok0 = cs.j * UT;
+    const bool ragged = unit_tok0 + UT > ctx_s;
+    const int lane_tok0 = unit_tok0 + (FP8 ? 16 : 8) * lj;  // first unit token of this lane's scores
 
-    constexpr int NZ = FP8 ? 8 : 4;  // scores per lane: bf16 tokens 4lj+r ; fp8 tokens 8lj+e
+    // S^T = K Q^T: lane (li, lj) holds scores of head li for its NZ tokens
     float z[NZ];
     if constexpr (FP8) {
-      for (int qg = 0; qg < 2; ++qg) {
+      for (int m = 0; m < 4; ++m) {
         f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
-        for (int hh = 0; hh < 2; ++hh) {
-          const i32x4 raw = kraw[2 * qg + hh];
-          const bf16x8 k0 = fp8x8_to_bf16(raw[0], raw[1]);
-          const bf16x8 k1 = fp8x8_to_bf16(raw[2], raw[3]);
-          sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0, __builtin_bit_cast(bf16x8, qcur[2 * hh]), sacc, 0, 0,
+        for (int jj = 0; jj < 2; ++jj) {
+          const i32x4 raw = R.k[2 * m + jj];
+          sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(raw[0], raw[1]),
+                                                         __builtin_bit_cast(bf16x8, qv[2 * jj]), sacc, 0, 0, 0);
+          sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(raw[2], raw[3]),
+                                                         __builtin_bit_cast(bf16x8, qv[2 * jj + 1]), sacc, 0, 0,
                                                          0);
-          sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1, __builtin_bit_cast(bf16x8, qcur[2 * hh + 1]), sacc, 0,
-                                                         0, 0);
         }
-        for (int r = 0; r < 4; ++r) z[4 * qg + r] = sacc[r] * cscale;
+        for (int e = 0; e < 4; ++e) z[4 * m + e] = sacc[e] * cscale;
       }
-      if (ragged)
-        for (int e = 0; e < 8; ++e)
-          if (unit_tok0 + 8 * lj + e >= ctx_s) z[e] = -INFINITY;
     } else {
-      f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
-      for (int c = 0; c < 4; ++c)
-        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kraw[c]),
-                                                       __builtin_bit_cast(bf16x8, qcur[c]), sacc, 0, 0, 0);
-      for (int r = 0; r < 4; ++r) z[r] = sacc[r] * cscale;
-      if (ragged)
-        for (int r = 0; r < 4; ++r)
-          if (unit_tok0 + 4 * lj + r >= ctx_s) z[r] = -INFINITY;
+      for (int m = 0; m < 2; ++m) {
+        f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
+        for (int c = 0; c < 4; ++c)
+          sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, R.k[4 * m + c]),
+                                                         __builtin_bit_cast(bf16x8, qv[c]), sacc, 0, 0, 0);
+        for (int e = 0; e < 4; ++e) z[4 * m + e] = sacc[e] * cscale;
+      }
     }
+    if (ragged)
+      for (int e = 0; e < NZ; ++e)
+        if (lane_tok0 + e >= ctx_s) z[e] = -INFINITY;
 
     // online softmax (base 2) for head li over this unit's tokens
     float bmax = z[0];
     for (int e = 1; e < NZ; ++e) bmax = fmaxf(bmax, z[e]);
     bmax = xor_max(bmax);
     const float m_new = fmaxf(m_run, bmax);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
-    __bf16 pb[NZ];
+    if (__builtin_amdgcn_ballot_w64(m_new > m_run) != 0) {  // some head's max grew: rescale
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      l_part *= alpha;
+      for (int nn = 0; nn < 8; ++nn) acc[nn] *= alpha;
+      m_run = m_new;
+    }
+    bf16x8 p[NZ / 8];
     float psum = 0.f;
     for (int e = 0; e < NZ; ++e) {
-      pb[e] = (__bf16)__builtin_amdgcn_exp2f(z[e] - m_new);
-      psum += (float)pb[e];
+      const __bf16 pe = (__bf16)__builtin_amdgcn_exp2f(z[e] - m_run);
+      p[e >> 3][e & 7] = pe;
+      psum += (float)pe;
     }
-    l_part = l_part * alpha + psum;
-    for (int nn = 0; nn < 8; ++nn) acc[nn] *= alpha;
+    l_part += psum;
 
-    wait_unit<D, LPU, 0>(younger);  // V tiles of this unit have landed
-
+    // O^T += V^T P^T
+    const int nv = ragged ? min(max(ctx_s - lane_tok0, 0), NZ) : NZ;  // live tokens of this lane's V fragment
     if constexpr (FP8) {
-      bf16x8 pop;
-      for (int e = 0; e < 8; ++e) pop[e] = pb[e];
-      i32x2 raw[8];
-      ds_read_tr8_x8(st, voff, raw);
       for (int nn = 0; nn < 8; ++nn) {
-        bf16x8 vop = fp8x8_to_bf16(raw[nn][0], raw[nn][1]);
-        if (ragged)
-          for (int e = 0; e < 8; ++e)
-            if (unit_tok0 + 8 * lj + e >= ctx_s) vop[e] = (__bf16)0.f;
-        acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pop, acc[nn], 0, 0, 0);
+        const i32x4 raw = R.v[nn];
+        bf16x8 vlo = fp8x8_to_bf16(raw[0], raw[1]);
+        bf16x8 vhi = fp8x8_to_bf16(raw[2], raw[3]);
+        if (ragged) {
+          vlo = keep_first(vlo, nv);
+          vhi = keep_first(vhi, nv - 8);
+        }
+        acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vlo, p[0], acc[nn], 0, 0, 0);
+        acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vhi, p[1], acc[nn], 0, 0, 0);
       }
     } else {
-      bf16x4 pop;
-      for (int e = 0; e < 4; ++e) pop[e] = pb[e];
-      i32x2 raw[8];
-      ds_read_tr16_x8(st, voff, raw);
       for (int nn = 0; nn < 8; ++nn) {
-        bf16x4 vop = __builtin_bit_cast(bf16x4, raw[nn]);
-        if (ragged)
-          for (int e = 0; e < 4; ++e)
-            if (unit_tok0 + 4 * lj + e >= ctx_s) vop[e] = (__bf16)0.f;
-        acc[nn] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vop, pop, acc[nn], 0, 0, 0);
+        bf16x8 vv = __builtin_bit_cast(bf16x8, R.v[nn]);
+        if (ragged) vv = keep_first(vv, nv);
+        acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vv, p[0], acc[nn], 0, 0, 0);
       }
     }
+  };
 
-    // ---- end of a piece: write the result or a partial record ----
-    const bool seg_end = cs_j == cs_nus - 1;
-    if (seg_end || ui == n - 1) {
-      const float l_tot = xor_sum(l_part);
-      const float inv = vsc / l_tot;
+  // End of a piece: write the rows or a partial record.
+  auto finish_piece = [&](int ui) {
+    const bool seg_end = cs.j == cs.nus - 1;
+    if (!(seg_end || ui == n - 1)) return;
+    const float l_tot = xor_sum(l_part);
+    const float inv = vsc / l_tot;
+    if (piece_j0 == 0 && seg_end) {  // the whole segment: final output
       if (li < G) {
-        if (piece_j0 == 0 && seg_end) {  // the whole segment: final output
-          const size_t row = ((size_t)cs_s * a.hq + cs_g * G + li) * kHeadDim;
-          for (int nn = 0; nn < 8; ++nn) {
-            const f32x4 o = acc[nn] * inv;
-            const size_t off = row + 16 * nn + 4 * lj;
-            if (a.out_fp32) {
-              *(f32x4*)((float*)a.out + off) = o;
-            } else {
-              u16x4 ob;
-              for (int e = 0; e < 4; ++e) ob[e] = f32_to_bf16_bits(o[e]);
-              *(u16x4*)((uint16_t*)a.out + off) = ob;
-            }
-          }
-        } else {  // a piece of a segment cut by slice boundaries
-          const size_t rec = (size_t)gw * 2 + (piece_first ? 0 : 1);
-          float* ro = a.rec_o + (rec * G + li) * kHeadDim;
-          for (int nn = 0; nn < 8; ++nn) *(f32x4*)(ro + 16 * nn + 4 * lj) = acc[nn] * inv;
-          if (lj == 0) {
-            a.rec_ml[(rec * G + li) * 2 + 0] = m_run;
-            a.rec_ml[(rec * G + li) * 2 + 1] = l_tot;
+        const size_t row = ((size_t)cs.s * a.hq + (size_t)cs.g * G + li) * kHeadDim;
+        for (int nn = 0; nn < 8; ++nn) {
+          const f32x4 o = acc[nn] * inv;
+          const size_t off = row + 16 * nn + 4 * lj;
+          if (a.out_fp32) {
+            *(f32x4*)((float*)a.out + off) = o;
+          } else {
+            u16x4 ob;
+            for (int e = 0; e < 4; ++e) ob[e] = f32_to_bf16_bits(o[e]);
+            *(u16x4*)((uint16_t*)a.out + off) = ob;
           }
         }
       }
-    }
-    // advance the compute-side position
-    if (ui + 1 < n) {
-      if (++cs_j == cs_nus) {
-        cs_j = 0;
-        if (++cs_g == Hkv) {
-          cs_g = 0;
-          do {
-            ++cs_s;
-          } while (cs_s < B - 1 && pre[cs_s + 1] == pre[cs_s]);  // skip empty sequences (bounded)
-          cs_s = __builtin_amdgcn_readfirstlane(cs_s);
-        }
-        cs_nus = __builtin_amdgcn_readfirstlane(pre[cs_s + 1] - pre[cs_s]);
+    } else {  // a piece of a segment cut by slice boundaries
+      const size_t rec = (size_t)gw * 2 + (piece_first ? 0 : 1);
+      if (li < G) {
+        float* ro = a.rec_o + (rec * G + li) * kHeadDim;
+        for (int nn = 0; nn < 8; ++nn) coherent_store4(ro + 16 * nn + 4 * lj, acc[nn] * inv);
+        if (lj == 0) coherent_store2(a.rec_ml + (rec * G + li) * 2, m_run, l_tot);
       }
-    }
-  }
-}
-
-// Log-sum-exp merge of the pieces of every segment cut by slice boundaries,
-// and zero rows for empty sequences.  One workgroup per wave of the stream
-// kernel: workgroup k merges the segment that wave k terminates (if any).
-// That segment covers units [a0, a0 + nus); slices have length C, so its
-// pieces come from waves k0 = a0 / C .. k: wave k0's last piece (record slot
-// 1 if that wave began inside an earlier segment, else slot 0) and the first
-// piece (slot 0) of every later wave.  256 threads = record groups x G heads
-// x 8 lanes of 16 head-dim values; each group folds its records with a
-// running log-sum-exp, and the groups are combined in LDS:
-// M = max_p m_p, w_p = l_p 2^(m_p - M), out = sum_p w_p o_p / sum_p w_p.
-__global__ __launch_bounds__(256) void paged_decode_merge_kernel(StreamArgs a) {
-  const int k = blockIdx.x;
-  const int G = a.group, B = a.batch;
-  const int tid = threadIdx.x;
-  // independent loads first: this wave's header, the slice length, and the
-  // prefix entries that say whether sequence k is empty
-  const i32x4 h = *(const i32x4*)(a.hdr + 4 * k);
-  const int C = a.plan[B + 1];
-  for (int s = k; s < B; s += gridDim.x) {  // empty sequences: zero rows
-    if (a.plan[s + 1] == a.plan[s]) {
-      for (int idx = tid; idx < a.hq * 32; idx += 256) {
-        const size_t o = (size_t)s * a.hq * kHeadDim + (size_t)idx * 4;
-        if (a.out_fp32) *(f32x4*)((float*)a.out + o) = f32x4{0.f, 0.f, 0.f, 0.f};
-        else *(u16x4*)((uint16_t*)a.out + o) = u16x4{0, 0, 0, 0};
-      }
-    }
-  }
-  const int s = h[0], g = h[1], a0 = h[2], nus = h[3];
-  if (nus == 0) return;  // wave k terminates no split segment
-  const int k0 = a0 / C;
-  const int first_slot = k0 * 2 + (a0 > k0 * C ? 1 : 0);
-  const int nrec = k - k0 + 1;
-  const int groups = 256 / (8 * G);             // G <= 16: at least 2 groups
-  const int grp = tid / (8 * G);
-  const int i = (tid >> 3) % G;                  // head inside the group
-  const int d0 = (tid & 7) * 16;                 // 16 head-dim values per lane
-  float m_run = -INFINITY, l_run = 0.f;
-  f32x4 acc[4] = {};
-  if (grp < groups) {
-    constexpr int kBatch = 8;  // records whose loads are in flight together
-    for (int r0 = grp; r0 < nrec; r0 += groups * kBatch) {
-      float m[kBatch], l[kBatch];
-      f32x4 o[kBatch][4];
-#pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        const int r = r0 + u * groups;
-        if (r < nrec) {
-          const size_t rec = r == 0 ? (size_t)first_slot : (size_t)(k0 + r) * 2;
-          const float* ml = a.rec_ml + (rec * G + i) * 2;
-          m[u] = ml[0];
-          l[u] = ml[1];
-          const f32x4* op = (const f32x4*)(a.rec_o + (rec * G + i) * kHeadDim + d0);
-          for (int e = 0; e < 4; ++e) o[u][e] = op[e];
-        } else {
-          m[u] = -INFINITY;
-          l[u] = 0.f;
-          for (int e = 0; e < 4; ++e) o[u][e] = f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        if (m[u] == -INFINITY) continue;
-        const float m_new = fmaxf(m_run, m[u]);
-        const float c_old = __builtin_amdgcn_exp2f(m_run - m_new);
-        const float c_new = l[u] * __builtin_amdgcn_exp2f(m[u] - m_new);
-        for (int e = 0; e < 4; ++e) acc[e] = acc[e] * c_old + o[u][e] * c_new;
-        l_run = l_run * c_old + c_new;
-        m_run = m_new;
-      }
-    }
-  }
-  __shared__ float sm[32][16], sl[32][16];
-  __shared__ f32x4 sacc[256][4];
-  if (grp < groups) {
-    if ((tid & 7) == 0) {
-      sm[grp][i] = m_run;
-      sl[grp][i] = l_run;
-    }
-    for (int e = 0; e < 4; ++e) sacc[tid][e] = acc[e];
-  }
-  __syncthreads();
-  if (grp == 0) {
-    float M = -INFINITY;
-    for (int q = 0; q < groups; ++q) M = fmaxf(M, sm[q][i]);
-    float L = 0.f;
-    f32x4 o[4] = {};
-    for (int q = 0; q < groups; ++q) {
-      const float c = sm[q][i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sm[q][i] - M);
-      L += sl[q][i] * c;
-      for (int e = 0; e < 4; ++e) o[e] += sacc[q * 8 * G + tid][e] * c;
-    }
-    const float inv = 1.0f / L;
-    const size_t orow = ((size_t)s * a.hq + (size_t)g * G + i) * kHeadDim + d0;
-    for (int e = 0; e < 4; ++e) {
-      const f32x4 v = o[e] * inv;
-      if (a.out_fp32) {
-        *(f32x4*)((float*)a.out + orow + 4 * e) = v;
+      if (piece_first) {
+        arr_s0 = cs.s;
+        arr_g0 = cs.g;
       } else {
-        u16x4 ob;
-        for (int q = 0; q < 4; ++q) ob[q] = f32_to_bf16_bits(v[q]);
-        *(u16x4*)((uint16_t*)a.out + orow + 4 * e) = ob;
+        arr_s1 = cs.s;
+        arr_g1 = cs.g;
       }
+    }
+  };
+
+  // One unit in flight while the previous one is computed.  The loop is
+  // unrolled by two so that both register buffers are static, and the last
+  // unit is peeled off so that every load inside the loop is unconditional.
+  // Program order of the loads: KV(u+1), then (if u+1 starts a segment)
+  // Q(u+1) once unit u no longer needs the previous group.
+  Walker nx = cs;  // position of the unit after the one being computed
+  advance(nx);
+  UnitRegs RA, RB;
+  load_q(qv, cs.s, cs.g);
+  issue(RA, 0);
+  auto step = [&](UnitRegs& cur, UnitRegs& nxt, int ui) {
+    issue(nxt, ui + 1);
+    begin_piece(ui);
+    compute_unit(cur);
+    finish_piece(ui);
+    if (nx.j == 0) load_q(qv, nx.s, nx.g);
+    cs = nx;
+    advance(nx);
+  };
+  auto last = [&](UnitRegs& cur, int ui) {
+    begin_piece(ui);
+    compute_unit(cur);
+    finish_piece(ui);
+  };
+  int ui = 0;
+  for (;;) {
+    if (ui + 1 >= n) {
+      last(RA, ui);
+      break;
+    }
+    step(RA, RB, ui++);
+    if (ui + 1 >= n) {
+      last(RB, ui);
+      break;
+    }
+    step(RB, RA, ui++);
+  }
+
+  // ---- 5. signal split pieces; the last arrivers merge them ----
+  if (arr_s0 >= 0 || arr_s1 >= 0) {
+    // this wave's record stores have completed (at the coherence point)
+    // before it counts them
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    int* const group_cnt = a.arrivals;
+    int* const seg_cnt = a.arrivals + TW;
+    for (int x = 0; x < 2; ++x) {
+      const int s = x == 0 ? arr_s0 : arr_s1;
+      if (s < 0) continue;
+      const int g = x == 0 ? arr_g0 : arr_g1;
+      const int nus = pre[s + 1] - pre[s];
+      const int a0 = Hkv * pre[s] + g * nus;  // first unit of the segment in the stream
+      const int k0 = a0 / C, kend = (a0 + nus - 1) / C;
+      const int np = kend - k0 + 1;           // piece r is wave k0 + r's
+      const int first_slot = 2 * k0 + (a0 > k0 * C ? 1 : 0);
+      auto piece_slot = [&](int r) { return r == 0 ? (size_t)first_slot : (size_t)2 * (k0 + r); };
+      const int r = gw - k0;
+      const int gfirst = r - r % kFanIn;
+      const int gn = min(np, gfirst + kFanIn) - gfirst;
+      const int kg = k0 + gfirst + gn - 1;    // wave of the group's last piece
+      const int ngroups = (np + kFanIn - 1) / kFanIn;
+      int old = 0;
+      if (lane == 0) old = __hip_atomic_fetch_add(group_cnt + kg, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      old = __shfl(old, 0);
+      if (old != gn - 1) continue;  // not the group's last arrival
+      asm volatile("" ::: "memory");  // record loads are issued after this branch resolves
+      if (lane == 0) __hip_atomic_store(group_cnt + kg, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (ngroups == 1) {
+        merge_records(a, piece_slot, np, true, s, g, 0, lane);
+        continue;
+      }
+      merge_records(a, [&](int i) { return piece_slot(gfirst + i); }, gn, false, s, g, (size_t)2 * TW + kg, lane);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      if (lane == 0) old = __hip_atomic_fetch_add(seg_cnt + kend, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      old = __shfl(old, 0);
+      if (old != ngroups - 1) continue;
+      asm volatile("" ::: "memory");
+      if (lane == 0) __hip_atomic_store(seg_cnt + kend, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      auto group_slot = [&](int c) {
+        return (size_t)2 * TW + k0 + min(np, (c + 1) * kFanIn) - 1;
+      };
+      merge_records(a, group_slot, ngroups, true, s, g, 0, lane);
     }
   }
 }
 
-// The instantiations the launcher dispatches to (bf16 / fp8 KV, 1-3 units in flight).
-template __global__ void paged_decode_stream_kernel<false, 1>(StreamArgs);
-template __global__ void paged_decode_stream_kernel<true, 1>(StreamArgs);
-template __global__ void paged_decode_stream_kernel<false, 2>(StreamArgs);
-template __global__ void paged_decode_stream_kernel<true, 2>(StreamArgs);
-template __global__ void paged_decode_stream_kernel<false, 3>(StreamArgs);
-template __global__ void paged_decode_stream_kernel<true, 3>(StreamArgs);
+template __global__ void paged_decode_kernel<false>(DecodeArgs);
+template __global__ void paged_decode_kernel<true>(DecodeArgs);
 
 }  // namespace dpool_hip
 
@@ -694,49 +707,32 @@ int device_cus(int* dev_out) {
   return cached[dev];
 }
 
-const void* stream_kernel(bool fp8, int d) {
-  switch (d * 2 + (fp8 ? 1 : 0)) {
-    case 2: return (const void*)paged_decode_stream_kernel<false, 1>;
-    case 3: return (const void*)paged_decode_stream_kernel<true, 1>;
-    case 4: return (const void*)paged_decode_stream_kernel<false, 2>;
-    case 5: return (const void*)paged_decode_stream_kernel<true, 2>;
-    case 6: return (const void*)paged_decode_stream_kernel<false, 3>;
-    default: return (const void*)paged_decode_stream_kernel<true, 3>;
-  }
-}
-
-// Workgroups of the stream kernel one compute unit holds at once, limited by
-// registers (runtime occupancy query, cached) and by LDS.  Without a device,
-// only the LDS limit applies.
-int blocks_per_cu(int dev, bool fp8, int d, size_t lds_bytes) {
+// Workgroups of the kernel one compute unit holds at once (register-limited;
+// runtime occupancy query, cached).  Without a device: 1.
+int resident_per_cu(int dev, bool fp8) {
   static std::mutex mu;
-  static int cached[64][2][4] = {};
-  int by_lds = (int)(kLdsBytes / lds_bytes);
-  if (dev < 0) return std::max(1, std::min(by_lds, 2));
-  int occ;
-  {
-    std::lock_guard<std::mutex> lock(mu);
-    occ = cached[dev][fp8 ? 1 : 0][d];
-    if (!occ) {
-      int n = 0;
-      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, stream_kernel(fp8, d), kWaves * 64, 0) != hipSuccess ||
-          n <= 0) {
-        (void)hipGetLastError();
-        n = 2;
-      }
-      occ = cached[dev][fp8 ? 1 : 0][d] = n;
+  static int cached[64][2] = {};
+  if (dev < 0) return 1;
+  std::lock_guard<std::mutex> lock(mu);
+  int& occ = cached[dev][fp8 ? 1 : 0];
+  if (!occ) {
+    int n = 0;
+    const void* fn = fp8 ? (const void*)paged_decode_kernel<true> : (const void*)paged_decode_kernel<false>;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, kWaves * 64, 0) != hipSuccess || n <= 0) {
+      (void)hipGetLastError();
+      n = 1;
     }
+    occ = n;
   }
-  return std::max(1, std::min(occ, by_lds));
+  return occ;
 }
 
 struct Plan {
-  int unit_tokens;   // tokens per unit (16 bf16, 32 fp8)
-  int min_chunk;     // minimum units per slice
-  int stages;
-  int grid;          // workgroups of the stream kernel
-  size_t dyn_lds;    // dynamic LDS bytes
-  size_t rec_o_off, rec_ml_off, plan_off, hdr_off, ws_bytes;
+  int unit_tokens;  // tokens per unit (32 bf16, 64 fp8)
+  int min_chunk;    // minimum units per slice
+  int grid;         // workgroups
+  size_t dyn_lds;   // dynamic LDS bytes
+  size_t arrivals_off, rec_ml_off, rec_o_off, ws_bytes;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -751,7 +747,7 @@ int validate(const dp_decode_shape* sh, Plan* plan) {
   if (sh->out_dtype != DP_OUT_BF16 && sh->out_dtype != DP_OUT_FP32)
     return fail(DP_ENOTSUP, "paged_decode: out_dtype %d", sh->out_dtype);
   if (sh->reserved != 0) return fail(DP_EINVAL, "paged_decode: reserved must be 0");
-  if (sh->batch < 0 || sh->batch > 65535) return fail(DP_EINVAL, "paged_decode: batch %d outside [0, 65535]", sh->batch);
+  if (sh->batch < 0) return fail(DP_EINVAL, "paged_decode: batch %d < 0", sh->batch);
   if (sh->batch > kMaxBatchInLds)
     return fail(DP_ENOTSUP, "paged_decode: batch %d > %d sequences per call", sh->batch, kMaxBatchInLds);
   if (sh->n_q_heads <= 0 || sh->n_kv_heads <= 0 || sh->n_kv_heads > 65535 || sh->n_q_heads % sh->n_kv_heads)
@@ -767,120 +763,41 @@ int validate(const dp_decode_shape* sh, Plan* plan) {
     return fail(DP_EINVAL, "paged_decode: num_blocks %lld (num_blocks * n_kv_heads must fit int32)",
                 (long long)sh->num_blocks);
   const bool fp8 = sh->kv_dtype == DP_KV_FP8_E4M3;
-  const int unit = fp8 ? 32 : 16;
+  const int unit = fp8 ? 64 : 32;
   const int P = sh->partition_tokens;
   if (P < 0 || P % unit || P / unit > kMaxUnitsPerWave)
     return fail(DP_EINVAL, "paged_decode: partition_tokens %d must be a multiple of %d in [0, %d]", P, unit,
                 unit * kMaxUnitsPerWave);
-  const int st = sh->pipeline_stages ? sh->pipeline_stages : 2;
-  if (st < 2 || st > 4) return fail(DP_EINVAL, "paged_decode: pipeline_stages %d outside [2, 4]", st);
+  const int wpc = sh->workgroups_per_cu;
+  if (wpc < 0 || wpc > 8) return fail(DP_EINVAL, "paged_decode: workgroups_per_cu %d outside [0, 8]", wpc);
   const int64_t units_per_seq = ((int64_t)sh->max_context_len + unit - 1) / unit;
   const int64_t max_units = units_per_seq * sh->batch * sh->n_kv_heads;
   if (max_units > INT32_MAX) return fail(DP_ENOTSUP, "paged_decode: %lld units exceed int32", (long long)max_units);
   plan->unit_tokens = unit;
-  plan->min_chunk = P ? P / unit : 8;
-  plan->stages = st;
-  // LDS per workgroup: K+V stages (8 KiB per unit) + tile indices + wave sums
-  // (static) + unit prefix, context lengths and fp8 scales (dynamic)
-  const size_t stat = (size_t)kWaves * st * 8192 + (size_t)kWaves * kMaxUnitsPerWave * (fp8 ? 2 : 1) * 4 + 64;
+  plan->min_chunk = P ? P / unit : 1;
+  // LDS per workgroup: tile lists + wave sums (static) + unit prefix,
+  // context lengths and fp8 scales (dynamic)
+  const size_t stat = (size_t)kWaves * kMaxUnitsPerWave * (fp8 ? 4 : 2) * 4 + 64;
   plan->dyn_lds = (size_t)(2 * sh->batch + 1 + 2 * sh->n_kv_heads) * 4;
-  const size_t lds = stat + plan->dyn_lds;
-  if (lds > kLdsBytes) return fail(DP_ENOTSUP, "paged_decode: %zu bytes of LDS per workgroup", lds);
+  if (stat + plan->dyn_lds > kLdsBytes)
+    return fail(DP_ENOTSUP, "paged_decode: %zu bytes of LDS per workgroup", stat + plan->dyn_lds);
   int dev = -1;
   const int cus = device_cus(&dev);
-  const int per_cu = blocks_per_cu(dev, fp8, st - 1, lds);
-  // persistent grid: every workgroup resident at once, and no slice longer
-  // than kMaxUnitsPerWave
+  const int per_cu = wpc ? std::min(wpc, resident_per_cu(dev, fp8)) : 1;
+  // persistent grid (every workgroup resident at once), grown only if some
+  // slice would exceed kMaxUnitsPerWave, shrunk when slices would be shorter
+  // than the minimum
   int64_t grid = (int64_t)cus * per_cu;
   const int64_t need = (max_units + (int64_t)kWaves * kMaxUnitsPerWave - 1) / ((int64_t)kWaves * kMaxUnitsPerWave);
-  grid = std::max(grid, need);
   const int64_t useful = (max_units + (int64_t)kWaves * plan->min_chunk - 1) / ((int64_t)kWaves * plan->min_chunk);
-  grid = std::max<int64_t>(1, std::min(grid, std::max(useful, need)));
+  grid = std::max<int64_t>(1, std::max(need, std::min(grid, useful)));
   plan->grid = (int)grid;
   const int G = sh->n_q_heads / sh->n_kv_heads;
-  const size_t recs = (size_t)grid * kWaves * 2 * G;
-  plan->rec_o_off = 0;
-  plan->rec_ml_off = align256(recs * kHeadDim * sizeof(float));
-  plan->plan_off = plan->rec_ml_off + align256(recs * 2 * sizeof(float));
-  plan->hdr_off = plan->plan_off + align256((size_t)(sh->batch + 2) * sizeof(int32_t));
-  plan->ws_bytes = plan->hdr_off + align256((size_t)grid * kWaves * 4 * sizeof(int32_t));
-  return DP_OK;
-}
-
-template <bool FP8, int ST>
-void launch_stream(const Plan& plan, hipStream_t stream, const StreamArgs& args) {
-  hipLaunchKernelGGL((paged_decode_stream_kernel<FP8, ST>), dim3(plan.grid), dim3(kWaves * 64), plan.dyn_lds,
-                     stream, args);
-}
-
-// Validate everything the host can check and fill the kernel arguments.
-int prepare(const void* q, const void* k_blocks, const void* v_blocks, const int32_t* block_tables,
-            const int32_t* context_lens, float scale, const float* k_scale, const float* v_scale, void* out,
-            const dp_decode_shape* shape, void* workspace, size_t workspace_bytes, Plan* plan, StreamArgs* args) {
-  using dpool::fail;
-  int rc = validate(shape, plan);
-  if (rc != DP_OK) return rc;
-  if (shape->batch == 0) return DP_OK;
-  if (!q || !k_blocks || !v_blocks || !block_tables || !context_lens || !out)
-    return fail(DP_EINVAL, "paged_decode: null tensor pointer");
-  const bool fp8 = shape->kv_dtype == DP_KV_FP8_E4M3;
-  if (fp8 && (!k_scale || !v_scale)) return fail(DP_EINVAL, "paged_decode: fp8 KV needs k_scale and v_scale");
-  if (!fp8 && (k_scale || v_scale)) return fail(DP_EINVAL, "paged_decode: k_scale/v_scale must be NULL for bf16 KV");
-  if (((uintptr_t)q | (uintptr_t)k_blocks | (uintptr_t)v_blocks | (uintptr_t)out) & 15)
-    return fail(DP_EINVAL, "paged_decode: q, k_blocks, v_blocks and out must be 16-byte aligned");
-  if (((uintptr_t)block_tables | (uintptr_t)context_lens) & 3)
-    return fail(DP_EINVAL, "paged_decode: block_tables and context_lens must be 4-byte aligned");
-  if (!std::isfinite(scale)) return fail(DP_EINVAL, "paged_decode: scale is not finite");
-  if (!workspace || workspace_bytes < plan->ws_bytes)
-    return fail(DP_ENOMEM, "paged_decode: workspace needs %zu bytes, got %zu", plan->ws_bytes, workspace_bytes);
-  if ((uintptr_t)workspace & 255) return fail(DP_EINVAL, "paged_decode: workspace must be 256-byte aligned");
-  StreamArgs& a = *args;
-  a.q = (const uint16_t*)q;
-  a.k = (const char*)k_blocks;
-  a.v = (const char*)v_blocks;
-  a.block_tables = block_tables;
-  a.context_lens = context_lens;
-  a.k_scale = k_scale;
-  a.v_scale = v_scale;
-  a.out = out;
-  a.rec_o = (float*)((char*)workspace + plan->rec_o_off);
-  a.rec_ml = (float*)((char*)workspace + plan->rec_ml_off);
-  a.plan = (int32_t*)((char*)workspace + plan->plan_off);
-  a.hdr = (int32_t*)((char*)workspace + plan->hdr_off);
-  a.qk_scale_log2 = scale * kLog2e;
-  a.batch = shape->batch;
-  a.hq = shape->n_q_heads;
-  a.hkv = shape->n_kv_heads;
-  a.group = shape->n_q_heads / shape->n_kv_heads;
-  a.max_blocks_per_seq = shape->max_blocks_per_seq;
-  a.max_ctx = shape->max_context_len;
-  a.num_blocks_m1 = (int32_t)(shape->num_blocks - 1);
-  a.out_fp32 = shape->out_dtype == DP_OUT_FP32;
-  a.min_chunk = plan->min_chunk;
-  return DP_OK;
-}
-
-int launch_partition_phase(const dp_decode_shape* shape, const Plan& plan, const StreamArgs& args, hipStream_t st) {
-  const bool fp8 = shape->kv_dtype == DP_KV_FP8_E4M3;
-  (void)hipGetLastError();  // clear a stale error left by earlier work
-  switch ((plan.stages - 1) * 2 + (fp8 ? 1 : 0)) {
-    case 2: launch_stream<false, 1>(plan, st, args); break;
-    case 3: launch_stream<true, 1>(plan, st, args); break;
-    case 4: launch_stream<false, 2>(plan, st, args); break;
-    case 5: launch_stream<true, 2>(plan, st, args); break;
-    case 6: launch_stream<false, 3>(plan, st, args); break;
-    default: launch_stream<true, 3>(plan, st, args); break;
-  }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return dpool::fail(DP_EIO, "paged_decode: stream kernel launch failed: %s", hipGetErrorString(e));
-  return DP_OK;
-}
-
-int launch_merge_phase(const Plan& plan, const StreamArgs& args, hipStream_t st) {
-  (void)hipGetLastError();
-  hipLaunchKernelGGL(paged_decode_merge_kernel, dim3(plan.grid * kWaves), dim3(256), 0, st, args);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return dpool::fail(DP_EIO, "paged_decode: merge launch failed: %s", hipGetErrorString(e));
+  const size_t waves = (size_t)grid * kWaves;
+  plan->arrivals_off = 0;
+  plan->rec_ml_off = align256(2 * waves * sizeof(int32_t));
+  plan->rec_o_off = plan->rec_ml_off + align256(3 * waves * G * 2 * sizeof(float));
+  plan->ws_bytes = plan->rec_o_off + align256(3 * waves * G * kHeadDim * sizeof(float));
   return DP_OK;
 }
 
@@ -903,55 +820,54 @@ extern "C" int paged_decode_attention(const void* q, const void* k_blocks, const
                                       const float* k_scale, const float* v_scale, void* out,
                                       const dp_decode_shape* shape, void* workspace, size_t workspace_bytes,
                                       void* stream) {
-  Plan plan;
-  StreamArgs args;
-  int rc = prepare(q, k_blocks, v_blocks, block_tables, context_lens, scale, k_scale, v_scale, out, shape, workspace,
-                   workspace_bytes, &plan, &args);
-  if (rc != DP_OK || shape->batch == 0) return rc;
-  rc = launch_partition_phase(shape, plan, args, (hipStream_t)stream);
-  if (rc != DP_OK) return rc;
-  return launch_merge_phase(plan, args, (hipStream_t)stream);
-}
-
-extern "C" int paged_decode_partition(const void* q, const void* k_blocks, const void* v_blocks,
-                                      const int32_t* block_tables, const int32_t* context_lens, float scale,
-                                      const float* k_scale, const float* v_scale, void* out,
-                                      const dp_decode_shape* shape, void* workspace, size_t workspace_bytes,
-                                      void* stream) {
-  Plan plan;
-  StreamArgs args;
-  int rc = prepare(q, k_blocks, v_blocks, block_tables, context_lens, scale, k_scale, v_scale, out, shape, workspace,
-                   workspace_bytes, &plan, &args);
-  if (rc != DP_OK || shape->batch == 0) return rc;
-  return launch_partition_phase(shape, plan, args, (hipStream_t)stream);
-}
-
-extern "C" int paged_decode_merge(const int32_t* context_lens, void* out, const dp_decode_shape* shape,
-                                  void* workspace, size_t workspace_bytes, void* stream) {
   using dpool::fail;
   Plan plan;
   int rc = validate(shape, &plan);
   if (rc != DP_OK) return rc;
   if (shape->batch == 0) return DP_OK;
-  if (!context_lens || !out) return fail(DP_EINVAL, "paged_decode_merge: null tensor pointer");
-  if (((uintptr_t)out & 15) || ((uintptr_t)context_lens & 3))
-    return fail(DP_EINVAL, "paged_decode_merge: out must be 16-byte and context_lens 4-byte aligned");
+  if (!q || !k_blocks || !v_blocks || !block_tables || !context_lens || !out)
+    return fail(DP_EINVAL, "paged_decode: null tensor pointer");
+  const bool fp8 = shape->kv_dtype == DP_KV_FP8_E4M3;
+  if (fp8 && (!k_scale || !v_scale)) return fail(DP_EINVAL, "paged_decode: fp8 KV needs k_scale and v_scale");
+  if (!fp8 && (k_scale || v_scale)) return fail(DP_EINVAL, "paged_decode: k_scale/v_scale must be NULL for bf16 KV");
+  if (((uintptr_t)q | (uintptr_t)k_blocks | (uintptr_t)v_blocks | (uintptr_t)out) & 15)
+    return fail(DP_EINVAL, "paged_decode: q, k_blocks, v_blocks and out must be 16-byte aligned");
+  if (((uintptr_t)block_tables | (uintptr_t)context_lens) & 3)
+    return fail(DP_EINVAL, "paged_decode: block_tables and context_lens must be 4-byte aligned");
+  if (!std::isfinite(scale)) return fail(DP_EINVAL, "paged_decode: scale is not finite");
   if (!workspace || workspace_bytes < plan.ws_bytes)
-    return fail(DP_ENOMEM, "paged_decode_merge: workspace needs %zu bytes, got %zu", plan.ws_bytes, workspace_bytes);
-  if ((uintptr_t)workspace & 255) return fail(DP_EINVAL, "paged_decode_merge: workspace must be 256-byte aligned");
-  StreamArgs a = {};
-  a.rec_o = (float*)((char*)workspace + plan.rec_o_off);
-  a.rec_ml = (float*)((char*)workspace + plan.rec_ml_off);
-  a.plan = (int32_t*)((char*)workspace + plan.plan_off);
-  a.hdr = (int32_t*)((char*)workspace + plan.hdr_off);
+    return fail(DP_ENOMEM, "paged_decode: workspace needs %zu bytes, got %zu", plan.ws_bytes, workspace_bytes);
+  if ((uintptr_t)workspace & 255) return fail(DP_EINVAL, "paged_decode: workspace must be 256-byte aligned");
+  DecodeArgs a;
+  a.q = (const uint16_t*)q;
+  a.k = (const char*)k_blocks;
+  a.v = (const char*)v_blocks;
+  a.block_tables = block_tables;
   a.context_lens = context_lens;
+  a.k_scale = k_scale;
+  a.v_scale = v_scale;
   a.out = out;
+  a.arrivals = (int32_t*)((char*)workspace + plan.arrivals_off);
+  a.rec_ml = (float*)((char*)workspace + plan.rec_ml_off);
+  a.rec_o = (float*)((char*)workspace + plan.rec_o_off);
+  a.qk_scale_log2 = scale * kLog2e;
   a.batch = shape->batch;
   a.hq = shape->n_q_heads;
   a.hkv = shape->n_kv_heads;
   a.group = shape->n_q_heads / shape->n_kv_heads;
+  a.max_blocks_per_seq = shape->max_blocks_per_seq;
   a.max_ctx = shape->max_context_len;
+  a.num_blocks_m1 = (int32_t)(shape->num_blocks - 1);
   a.out_fp32 = shape->out_dtype == DP_OUT_FP32;
   a.min_chunk = plan.min_chunk;
-  return launch_merge_phase(plan, a, (hipStream_t)stream);
+  (void)hipGetLastError();  // clear a stale error left by earlier work
+  if (fp8)
+    hipLaunchKernelGGL(paged_decode_kernel<true>, dim3(plan.grid), dim3(kWaves * 64), plan.dyn_lds,
+                       (hipStream_t)stream, a);
+  else
+    hipLaunchKernelGGL(paged_decode_kernel<false>, dim3(plan.grid), dim3(kWaves * 64), plan.dyn_lds,
+                       (hipStream_t)stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(DP_EIO, "paged_decode: kernel launch failed: %s", hipGetErrorString(e));
+  return DP_OK;
 }

@@ -217,15 +217,15 @@ def shape(host_lib, **kw):
 def test_workspace_and_partition_sizes(host_lib):
     s = shape(host_lib)
     P = host_lib.partition_tokens(s)
-    assert P > 0 and P % 16 == 0
+    assert P > 0 and P % 32 == 0
     ws = host_lib.workspace_size(s)
     assert ws > 0 and ws % 256 == 0
-    # partial records (2 per wave, G heads of 130 floats) + the unit prefix
-    s2 = shape(host_lib, partition_tokens=16)
-    assert host_lib.partition_tokens(s2) == 16
-    assert host_lib.workspace_size(s2) >= 2 * 4 * 130 * 4
-    s3 = shape(host_lib, kv_fp8=True, partition_tokens=32)
-    assert host_lib.partition_tokens(s3) == 32
+    # per wave: two arrival counters + three partial records of G heads x 130 floats
+    s2 = shape(host_lib, partition_tokens=32)
+    assert host_lib.partition_tokens(s2) == 32
+    assert host_lib.workspace_size(s2) >= 8 + 3 * 4 * 130 * 4
+    s3 = shape(host_lib, kv_fp8=True, partition_tokens=64)
+    assert host_lib.partition_tokens(s3) == 64
     big = shape(host_lib, batch=4096, max_context_len=1000)
     assert host_lib.workspace_size(big) > 0
     assert host_lib.workspace_size(shape(host_lib, batch=4097)) == 0   # unit prefix is kept in LDS
@@ -234,9 +234,10 @@ def test_workspace_and_partition_sizes(host_lib):
 @pytest.mark.parametrize("kw,code", [
     (dict(head_dim=64), -95), (dict(block_size=32), -95), (dict(n_q_heads=12, n_kv_heads=8), -22),
     (dict(n_q_heads=64, n_kv_heads=2), -95), (dict(max_context_len=64 * 16 + 1), -22),
-    (dict(partition_tokens=24), -22), (dict(kv_fp8=True, partition_tokens=16), -22),
-    (dict(pipeline_stages=5), -22), (dict(num_blocks=0), -22), (dict(batch=70000), -22),
-    (dict(batch=5000), -95), (dict(partition_tokens=16 * 257), -22),
+    (dict(partition_tokens=24), -22), (dict(partition_tokens=16), -22),
+    (dict(kv_fp8=True, partition_tokens=32), -22), (dict(workgroups_per_cu=9), -22),
+    (dict(workgroups_per_cu=-1), -22), (dict(num_blocks=0), -22), (dict(batch=-1), -22),
+    (dict(batch=5000), -95), (dict(partition_tokens=32 * 257), -22),
 ])
 def test_invalid_shapes_rejected_on_host(host_lib, kw, code):
     s = shape(host_lib, **kw)
@@ -257,8 +258,10 @@ def test_bad_pointers_rejected_on_host(host_lib):
     sf = shape(host_lib, kv_fp8=True)
     assert L.paged_decode_attention(16, 16, 16, 16, 16, 1.0, None, None, 16, ctypes.byref(sf), 256, 10 ** 9,
                                     None) == -22
-    s16 = shape(host_lib, partition_tokens=16)
-    assert L.paged_decode_attention(16, 16, 16, 16, 16, 1.0, None, None, 16, ctypes.byref(s16), None, 0,
+    s32 = shape(host_lib, partition_tokens=32)
+    assert L.paged_decode_attention(16, 16, 16, 16, 16, 1.0, None, None, 16, ctypes.byref(s32), None, 0,
+                                    None) == -12
+    assert L.paged_decode_attention(16, 16, 16, 16, 16, 1.0, None, None, 16, ctypes.byref(s), 256, ws - 1,
                                     None) == -12
     assert L.paged_decode_attention(16, 16, 16, 16, 16, float("nan"), None, None, 16, ctypes.byref(s), 256, ws,
                                     None) == -22
@@ -267,8 +270,9 @@ def test_bad_pointers_rejected_on_host(host_lib):
 def test_decoder_wrapper_constructs_on_host(host_lib):
     dec = host_lib.PagedDecoder(4, 8, 2, 64, 1000, 300, partition_tokens=64, device="cpu")
     assert dec.partition_tokens == 64
-    assert callable(dec.partition) and callable(dec.merge) and callable(dec)
+    assert callable(dec)
     assert dec.workspace is not None and dec.workspace.numel() == host_lib.workspace_size(dec.shape)
+    assert int(dec.workspace.count_nonzero()) == 0     # the library needs a zero-filled workspace
     assert tuple(dec.new_out("cpu").shape) == (4, 8, 128)
     with pytest.raises(host_lib.DpoolError):
         host_lib.PagedDecoder(4, 8, 2, 64, 1000, 300, partition_tokens=24, device="cpu")

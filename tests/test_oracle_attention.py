@@ -20,7 +20,10 @@ def codes_bf16(x):
 
 
 def dense_case(rng, B, Hq, Hkv, ctx, nb_pool=None, vals=None, kv="bf16"):
-    """Small dense pool with a shuffled block table; values N(0,1) unless given."""
+    """Small dense pool with a shuffled block table; values N(0,1) unless given.
+
+    K and V are drawn token-major [nb, Hkv, 16, 128]; V is returned in the
+    interface's dims-major tile layout [nb, Hkv, 128, 16]."""
     nblk = [-(-c // 16) for c in ctx]
     used = sum(nblk)
     nb_pool = nb_pool or max(used * 2, 1)
@@ -35,13 +38,16 @@ def dense_case(rng, B, Hq, Hkv, ctx, nb_pool=None, vals=None, kv="bf16"):
     v = rng.standard_normal((nb_pool, Hkv, 16, 128)).astype(np.float32)
     if vals:
         q, k, v = vals(q, k, v, bt)
-    return codes_bf16(q), codes_bf16(k), codes_bf16(v), bt, np.asarray(ctx, np.int32)
+    vt = np.ascontiguousarray(codes_bf16(v).transpose(0, 1, 3, 2))
+    return codes_bf16(q), codes_bf16(k), vt, bt, np.asarray(ctx, np.int32)
 
 
-def dense_gather(pool_codes, bt, s, g, T, fmt="bf16"):
+def dense_gather(pool_codes, bt, s, g, T, fmt="bf16", dims_major=False):
+    """Token rows 0..T-1 of (sequence s, KV head g), one element lookup per row."""
     rows = []
     for t in range(T):
-        rows.append(numerics.decode(pool_codes[bt[s, t // 16], g, t % 16], fmt))
+        tile = pool_codes[bt[s, t // 16], g]
+        rows.append(numerics.decode(tile[:, t % 16] if dims_major else tile[t % 16], fmt))
     return np.array(rows).reshape(T, -1)
 
 
@@ -56,7 +62,8 @@ def sdpa_reference(qb, kb, vb, bt, ctx, scale, fmt="bf16", ks=None, vs=None):
         if T == 0:
             continue
         K = np.stack([dense_gather(kb, bt, s, g, T, fmt) * (1 if ks is None else ks[g]) for g in range(Hkv)])
-        V = np.stack([dense_gather(vb, bt, s, g, T, fmt) * (1 if vs is None else vs[g]) for g in range(Hkv)])
+        V = np.stack([dense_gather(vb, bt, s, g, T, fmt, dims_major=True) * (1 if vs is None else vs[g])
+                      for g in range(Hkv)])
         Kt = torch.from_numpy(K).repeat_interleave(G, dim=0)[None]   # [1, Hq, T, D]
         Vt = torch.from_numpy(V).repeat_interleave(G, dim=0)[None]
         Qt = torch.from_numpy(numerics.decode_bf16(qb[s]))[None, :, None, :]  # [1, Hq, 1, D]
@@ -91,7 +98,7 @@ def brute_force(qb, kb, vb, bt, ctx, scale):
                 num = 0.0
                 for t in range(T):
                     blk, slot = int(bt[s][t // 16]), t % 16
-                    num += w[t] * numerics.bf16_value(int(vb[blk, g, slot, i]))
+                    num += w[t] * numerics.bf16_value(int(vb[blk, g, i, slot]))
                 out[s][h][i] = num / den
     return np.array(out)
 
@@ -141,7 +148,7 @@ def test_one_token_returns_v0():
     got = run_oracle(qb, kb, vb, bt, cl)
     for s in range(3):
         for h in range(8):
-            assert np.array_equal(got[s, h], numerics.decode_bf16(vb[bt[s, 0], h // 4, 0]))
+            assert np.array_equal(got[s, h], numerics.decode_bf16(vb[bt[s, 0], h // 4, :, 0]))
 
 
 def test_constant_v_returns_v():
@@ -153,7 +160,7 @@ def test_constant_v_returns_v():
     qb, kb, vb, bt, cl = dense_case(rng, 2, 4, 2, [37, 64], vals=vals)
     got = run_oracle(qb, kb, vb, bt, cl)
     for h in range(4):
-        np.testing.assert_allclose(got[:, h], np.broadcast_to(numerics.decode_bf16(vb[0, h // 2, 0]), (2, 128)),
+        np.testing.assert_allclose(got[:, h], np.broadcast_to(numerics.decode_bf16(vb[0, h // 2, :, 0]), (2, 128)),
                                    rtol=0, atol=1e-14)
 
 
@@ -168,7 +175,7 @@ def test_identical_k_rows_give_mean_of_v():
     got = run_oracle(qb, kb, vb, bt, cl)
     for s, T in enumerate(ctx):
         for h in range(4):
-            mean = dense_gather(vb, bt, s, h // 2, T).mean(axis=0)
+            mean = dense_gather(vb, bt, s, h // 2, T, dims_major=True).mean(axis=0)
             np.testing.assert_allclose(got[s, h], mean, rtol=0, atol=1e-13)
 
 
@@ -178,7 +185,7 @@ def test_zero_scale_gives_mean_of_v():
     qb, kb, vb, bt, cl = dense_case(rng, 2, 4, 1, ctx)
     got = run_oracle(qb, kb, vb, bt, cl, scale=0.0)
     for s, T in enumerate(ctx):
-        mean = dense_gather(vb, bt, s, 0, T).mean(axis=0)
+        mean = dense_gather(vb, bt, s, 0, T, dims_major=True).mean(axis=0)
         for h in range(4):
             np.testing.assert_allclose(got[s, h], mean, rtol=0, atol=1e-13)
 

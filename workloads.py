@@ -32,6 +32,10 @@ are scattered.
 
 Draw order within one numpy Generator(seed): lengths, block-id permutation,
 Q, K, V.  Values are N(0, 1) float32 rounded to bf16 (round-to-nearest-even).
+Storage layout of one (block, KV head) tile: K token-major [16, 128], V
+dims-major [128, 16] (each head dimension's 16 tokens contiguous), as the
+library's interface specifies; the values are drawn token-major and V is
+transposed after rounding, so the draw does not depend on the layout.
 FP8 keys and values get one scale per KV head, amax / 448 over that head's
 live tokens, and are clamped to +-448 before rounding to e4m3 (torch's cast
 does not saturate).  With poison=True the slots past each sequence's last
@@ -106,7 +110,7 @@ def to_e4m3_codes(x: np.ndarray) -> np.ndarray:
 
 
 class BlockStore:
-    """Read-only view of a paged pool [num_blocks, Hkv, bs, D] of codes that only
+    """Read-only view of a paged pool [num_blocks, Hkv, ...tile] of codes that only
     materialises the blocks in use; unused blocks read back as NaN codes."""
 
     def __init__(self, used_ids: np.ndarray, tiles: np.ndarray, num_blocks: int, nan_code):
@@ -215,10 +219,11 @@ def make_workload(batch, n_q_heads, n_kv_heads, context_lens, c_max, kv_format="
     else:
         raise ValueError(kv_format)
     del k, v
+    v_codes = np.ascontiguousarray(v_codes.transpose(0, 1, 3, 2))   # [used, Hkv, D, bs]: dims-major V tiles
     if poison and used:
-        dead = ~live
-        k_codes[np.nonzero(dead)[0], :, np.nonzero(dead)[1], :] = nan
-        v_codes[np.nonzero(dead)[0], :, np.nonzero(dead)[1], :] = nan
+        dead_blk, dead_slot = np.nonzero(~live)
+        k_codes[dead_blk, :, dead_slot, :] = nan
+        v_codes[dead_blk, :, :, dead_slot] = nan
     return Workload(
         config=config, name=name, batch=batch, n_q_heads=n_q_heads, n_kv_heads=n_kv_heads,
         c_max=c_max, kv_format=kv_format, num_blocks=int(num_blocks), max_blocks_per_seq=max_blocks,
@@ -243,19 +248,20 @@ def make_config(i: int, seed: int | None = None, poison: bool = True) -> Workloa
 def to_device(w: Workload, device="cuda", layers: int = 1, poison_unused: bool = True):
     """Place a workload in device memory (torch tensors; plumbing only).
 
-    Returns a dict with q [B, Hq, D] (bf16 codes as int16), k/v pools
-    [layers, num_blocks, Hkv, bs, D] (int16 bf16 codes or uint8 e4m3 codes;
-    every layer holds the same tiles at the same block ids), block_tables,
+    Returns a dict with q [B, Hq, D] (bf16 codes as int16), k pools
+    [layers, num_blocks, Hkv, bs, D] and v pools [layers, num_blocks, Hkv, D, bs]
+    (int16 bf16 codes or uint8 e4m3 codes; every layer holds the same tiles at
+    the same block ids), block_tables,
     context_lens (int32) and the fp8 scales.  Unused pool blocks are NaN codes
     when poison_unused, else left unwritten.
     """
     fp8 = w.kv_format == "fp8_e4m3"
     tdt = torch.uint8 if fp8 else torch.int16
     nan = int(E4M3_NAN) if fp8 else int(np.int16(np.uint16(BF16_NAN).view(np.int16)))
-    shape = (layers, w.num_blocks, w.n_kv_heads, w.block_size, w.head_dim)
     ids = torch.from_numpy(w.k_store.used_ids).to(device)
     out = {}
     for name, store in (("k", w.k_store), ("v", w.v_store)):
+        shape = (layers,) + tuple(store.shape)
         pool = torch.full(shape, nan, dtype=tdt, device=device) if poison_unused else torch.empty(
             shape, dtype=tdt, device=device)
         tiles = torch.from_numpy(store.tiles.view(np.int16) if not fp8 else store.tiles).to(device)
