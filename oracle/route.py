@@ -19,7 +19,7 @@ OnResponse(r, k, prompt_tokens)                           (Algorithm 1, OnRespon
 
 Defaults: c0 = 4.0 (cold start), beta = 0.95, gamma = 1.0, B_short = 8192.
 
-Readings where the paper is silent (each also listed in the design doc):
+Readings where the paper is silent:
   * sigma starts at 0 (its initial value is not given).
   * c* is clamped below at c_min = 1.0 byte/token, so that gamma * sigma >= c_hat
     cannot give a zero or negative ratio.

@@ -446,7 +446,8 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     for (int x = 0; x < 8; ++x) R.v[x] = __builtin_nontemporal_load((const i32x4*)(vb + vofs[x]));
   };
 
-  i32x4 qv[4];  // query group of the piece being computed; reloaded right after a segment's last unit
+  i32x4 qv[4];  // query group of the piece being computed
+  i32x4 qn[4];  // query group of the next segment, loaded before that segment's first unit
   float m_run = -INFINITY, l_part = 0.f, cscale = 0.f, vsc = 1.0f;
   f32x4 acc[8];
   for (int nn = 0; nn < 8; ++nn) acc[nn] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -460,6 +461,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       piece_first = ui == 0;
       piece_j0 = cs.j;
       ctx_s = __builtin_amdgcn_readfirstlane(ctxs[cs.s]);
+      for (int c = 0; c < 4; ++c) qv[c] = qn[c];
       float ksc = 1.0f;
       if constexpr (FP8) {
         ksc = kscl[cs.g];
@@ -588,20 +590,21 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
 
   // One unit in flight while the previous one is computed.  The loop is
   // unrolled by two so that both register buffers are static, and the last
-  // unit is peeled off so that every load inside the loop is unconditional.
-  // Program order of the loads: KV(u+1), then (if u+1 starts a segment)
-  // Q(u+1) once unit u no longer needs the previous group.
+  // unit is peeled off so that every KV load inside the loop is
+  // unconditional.  Program order of the loads: Q(u+1) if u+1 starts a
+  // segment, then KV(u+1), then the computation of unit u; so waiting for a
+  // unit's query group never waits for the unit behind it.
   Walker nx = cs;  // position of the unit after the one being computed
   advance(nx);
   UnitRegs RA, RB;
-  load_q(qv, cs.s, cs.g);
+  load_q(qn, cs.s, cs.g);
   issue(RA, 0);
   auto step = [&](UnitRegs& cur, UnitRegs& nxt, int ui) {
-    issue(nxt, ui + 1);
     begin_piece(ui);
+    if (nx.j == 0) load_q(qn, nx.s, nx.g);
+    issue(nxt, ui + 1);
     compute_unit(cur);
     finish_piece(ui);
-    if (nx.j == 0) load_q(qv, nx.s, nx.g);
     cs = nx;
     advance(nx);
   };
@@ -610,18 +613,20 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     compute_unit(cur);
     finish_piece(ui);
   };
+  // Pairs of units while at least one more unit follows the pair, then the
+  // last one or two units.  (A loop with exits in the middle of its body
+  // makes the compiler's wait-count merge at the loop header conservative,
+  // and it then drains every load in flight once per iteration.)
   int ui = 0;
-  for (;;) {
-    if (ui + 1 >= n) {
-      last(RA, ui);
-      break;
-    }
-    step(RA, RB, ui++);
-    if (ui + 1 >= n) {
-      last(RB, ui);
-      break;
-    }
-    step(RB, RA, ui++);
+  for (; ui + 2 < n; ui += 2) {
+    step(RA, RB, ui);
+    step(RB, RA, ui + 1);
+  }
+  if (ui + 1 < n) {
+    step(RA, RB, ui);
+    last(RB, ui + 1);
+  } else {
+    last(RA, ui);
   }
 
   // ---- 5. signal split pieces; the last arrivers merge them ----
