@@ -71,6 +71,11 @@ constexpr int kBlock = 16;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kWaves = 4;              // waves per workgroup
 constexpr int kMaxUnitsPerWave = 256;  // the host sizes the grid so that no slice is longer
+// Finished output rows and partial records are staged in LDS and written out
+// after the loop (global stores share the in-order memory counter with the
+// KV loads; a store issued inside the loop would make the next wait cover it).
+constexpr int kStageBytes = 24 * 1024;  // per wave
+constexpr int kMaxStaged = 6;           // entries per wave
 
 struct DecodeArgs {
   const uint16_t* q;            // [B, Hq, 128] bf16
@@ -128,11 +133,15 @@ __device__ __forceinline__ bf16x8 fp8x8_to_bf16(int lo, int hi) {
   return r;
 }
 
-// Zero the elements at positions >= nv (0..8) of eight bf16.
-__device__ __forceinline__ bf16x8 keep_first(bf16x8 x, int nv) {
-  for (int e = 0; e < 8; ++e)
-    if (e >= nv) x[e] = (__bf16)0.f;
-  return x;
+// Mask of the live bytes of 32-bit word w of a V fragment whose first nv
+// tokens are live: tokens of `per_word` bytes each (2: bf16, 1: fp8), so a
+// word holds 4 / per_word tokens.  Dead tokens (past the context, possibly
+// NaN-poisoned slots) become +0.
+template <int kTokBytes>
+__device__ __forceinline__ unsigned live_mask(int w, int nv) {
+  constexpr int kPerWord = 4 / kTokBytes;
+  const int k = min(max(nv - kPerWord * w, 0), kPerWord);  // live tokens in this word
+  return k == kPerWord ? 0xffffffffu : (1u << (8 * kTokBytes * k)) - 1u;
 }
 
 __device__ __forceinline__ uint16_t f32_to_bf16_bits(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
@@ -279,6 +288,9 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   constexpr int UB = GE::UB, UT = GE::UT, TILE = GE::TILE, NZ = GE::NZ;
   __shared__ int tiles_lds[kWaves][kMaxUnitsPerWave * UB];
   __shared__ int wave_sums[kWaves];
+  __shared__ __attribute__((aligned(16))) char stage_lds[kWaves][kStageBytes];
+  __shared__ long long stage_dst[kWaves][kMaxStaged];  // element offset of a row in `out`, or a record slot
+  __shared__ int stage_kind[kWaves][kMaxStaged];       // 0 bf16 row, 1 fp32 row, 2 record
   extern __shared__ int dyn[];  // pre[B + 1], ctxs[B], k_scale[Hkv], v_scale[Hkv]
 
   const int lane = threadIdx.x & 63;
@@ -418,7 +430,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     cs.g = __builtin_amdgcn_readfirstlane(r / cs.nus);
     cs.j = __builtin_amdgcn_readfirstlane(r - cs.g * cs.nus);
   }
-  auto advance = [&](Walker& wk) {
+  auto advance = [&](Walker& wk) __attribute__((always_inline)) {
     if (++wk.j == wk.nus) {
       wk.j = 0;
       if (++wk.g == Hkv) {
@@ -431,13 +443,13 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       wk.nus = __builtin_amdgcn_readfirstlane(pre[wk.s + 1] - pre[wk.s]);
     }
   };
-  // Every load below is unconditional, so the compiler's wait counts stay
-  // exact: a wait for one unit never drains the unit behind it.
-  auto load_q = [&](i32x4 (&qr)[4], int s, int g) {
+  // Every load in the loop is unconditional, so the compiler's wait counts
+  // stay exact: a wait for one unit never drains the unit behind it.
+  auto load_q = [&](i32x4 (&qr)[4], int s, int g) __attribute__((always_inline)) {
     const uint16_t* qrow = a.q + ((size_t)s * a.hq + (size_t)g * G + qhead) * kHeadDim;
     for (int c = 0; c < 4; ++c) qr[c] = *(const i32x4*)(qrow + qoff[c]);
   };
-  auto issue = [&](UnitRegs& R, int ui) {
+  auto issue = [&](UnitRegs& R, int ui) __attribute__((always_inline)) {
     const char* kb = a.k + (size_t)tiles[ui * UB + kblk] * TILE;
     const char* vb = a.v + (size_t)tiles[ui * UB + vblk] * TILE;
 #pragma unroll
@@ -446,8 +458,56 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     for (int x = 0; x < 8; ++x) R.v[x] = __builtin_nontemporal_load((const i32x4*)(vb + vofs[x]));
   };
 
-  i32x4 qv[4];  // query group of the piece being computed
-  i32x4 qn[4];  // query group of the next segment, loaded before that segment's first unit
+  // ---- staging of finished rows and records in LDS ----
+  // Entry layout: eight 16-byte (fp32) or 8-byte (bf16) chunks per lane,
+  // chunk-major ([nn][lane]), then for a record each lane's (m, l).
+  char* const stg = stage_lds[w];
+  int st_n = 0, st_off = 0;  // entries and bytes staged (wave-uniform)
+  auto flush = [&]() __attribute__((always_inline)) {
+    for (int e = 0; e < st_n; ++e) {
+      const int ko = __builtin_amdgcn_readfirstlane(stage_kind[w][e]);
+      const int kind = ko & 15;
+      const char* base = stg + (ko >> 4);
+      const long long dst = stage_dst[w][e];
+      const unsigned dlo = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)(dst & 0xffffffffll));
+      const unsigned dhi = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)((unsigned long long)dst >> 32));
+      const size_t d = ((size_t)dhi << 32) | dlo;
+      if (li >= G) continue;
+      if (kind == 2) {  // partial record, slot d
+        float* ro = a.rec_o + (d * G + li) * kHeadDim;
+        for (int nn = 0; nn < 8; ++nn) coherent_store4(ro + 16 * nn + 4 * lj, *(const f32x4*)(base + nn * 1024 + lane * 16));
+        if (lj == 0) {
+          const float* ml = (const float*)(base + 8192 + lane * 8);
+          coherent_store2(a.rec_ml + (d * G + li) * 2, ml[0], ml[1]);
+        }
+      } else {  // output rows of one (sequence, KV head): d is the element offset of its first row
+        const size_t row = d + (size_t)li * kHeadDim;
+        for (int nn = 0; nn < 8; ++nn) {
+          const size_t off = row + 16 * nn + 4 * lj;
+          if (kind == 1) *(f32x4*)((float*)a.out + off) = *(const f32x4*)(base + nn * 1024 + lane * 16);
+          else *(u16x4*)((uint16_t*)a.out + off) = *(const u16x4*)(base + nn * 512 + lane * 8);
+        }
+      }
+    }
+    st_n = 0;
+    st_off = 0;
+  };
+  auto stage_begin = [&](int bytes) __attribute__((always_inline)) {  // room for one entry; returns its LDS offset
+    if (st_n == kMaxStaged || st_off + bytes > kStageBytes) flush();
+    const int off = st_off;
+    st_off += bytes;
+    return off;
+  };
+  auto stage_meta = [&](int kind, int off, long long dst) __attribute__((always_inline)) {
+    if (lane == 0) {
+      stage_kind[w][st_n] = kind | (off << 4);
+      stage_dst[w][st_n] = dst;
+    }
+    ++st_n;
+  };
+
+  i32x4 qv[4];          // query group of the piece being computed
+  i32x4 qE[4], qO[4];   // query groups of the segments of the next even / odd unit
   float m_run = -INFINITY, l_part = 0.f, cscale = 0.f, vsc = 1.0f;
   f32x4 acc[8];
   for (int nn = 0; nn < 8; ++nn) acc[nn] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -456,12 +516,13 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   // split segments this wave must signal: (s, g) of its first piece and of its last piece, s = -1 if none
   int arr_s0 = -1, arr_g0 = 0, arr_s1 = -1, arr_g1 = 0;
 
-  auto begin_piece = [&](int ui) {
+  auto begin_piece = [&](int ui, const i32x4 (&qs)[4]) __attribute__((always_inline)) {
     if (ui == 0 || cs.j == 0) {  // a new piece starts: its query group, fresh softmax state
       piece_first = ui == 0;
       piece_j0 = cs.j;
       ctx_s = __builtin_amdgcn_readfirstlane(ctxs[cs.s]);
-      for (int c = 0; c < 4; ++c) qv[c] = qn[c];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) qv[c] = qs[c];
       float ksc = 1.0f;
       if constexpr (FP8) {
         ksc = kscl[cs.g];
@@ -470,11 +531,12 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       cscale = a.qk_scale_log2 * ksc;
       m_run = -INFINITY;
       l_part = 0.f;
+#pragma unroll
       for (int nn = 0; nn < 8; ++nn) acc[nn] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
   };
 
-  auto compute_unit = [&](const UnitRegs& R) {
+  auto compute_unit = [&](const UnitRegs& R) __attribute__((always_inline)) {
     const int unit_tok0 = cs.j * UT;
     const bool ragged = unit_tok0 + UT > ctx_s;
     const int lane_tok0 = unit_tok0 + (FP8 ? 16 : 8) * lj;  // first unit token of this lane's scores
@@ -482,8 +544,10 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     // S^T = K Q^T: lane (li, lj) holds scores of head li for its NZ tokens
     float z[NZ];
     if constexpr (FP8) {
+#pragma unroll
       for (int m = 0; m < 4; ++m) {
         f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
         for (int jj = 0; jj < 2; ++jj) {
           const i32x4 raw = R.k[2 * m + jj];
           sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(raw[0], raw[1]),
@@ -492,20 +556,27 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
                                                          __builtin_bit_cast(bf16x8, qv[2 * jj + 1]), sacc, 0, 0,
                                                          0);
         }
+#pragma unroll
         for (int e = 0; e < 4; ++e) z[4 * m + e] = sacc[e] * cscale;
       }
     } else {
+#pragma unroll
       for (int m = 0; m < 2; ++m) {
         f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
         for (int c = 0; c < 4; ++c)
           sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, R.k[4 * m + c]),
                                                          __builtin_bit_cast(bf16x8, qv[c]), sacc, 0, 0, 0);
+#pragma unroll
         for (int e = 0; e < 4; ++e) z[4 * m + e] = sacc[e] * cscale;
       }
     }
+    // live tokens among this lane's NZ tokens (all of them unless the unit is ragged)
+    const int nv = ragged ? min(max(ctx_s - lane_tok0, 0), NZ) : NZ;
     if (ragged)
+#pragma unroll
       for (int e = 0; e < NZ; ++e)
-        if (lane_tok0 + e >= ctx_s) z[e] = -INFINITY;
+        if (e >= nv) z[e] = -INFINITY;
 
     // online softmax (base 2) for head li over this unit's tokens
     float bmax = z[0];
@@ -515,11 +586,13 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     if (__builtin_amdgcn_ballot_w64(m_new > m_run) != 0) {  // some head's max grew: rescale
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
       l_part *= alpha;
+#pragma unroll
       for (int nn = 0; nn < 8; ++nn) acc[nn] *= alpha;
       m_run = m_new;
     }
     bf16x8 p[NZ / 8];
     float psum = 0.f;
+#pragma unroll
     for (int e = 0; e < NZ; ++e) {
       const __bf16 pe = (__bf16)__builtin_amdgcn_exp2f(z[e] - m_run);
       p[e >> 3][e & 7] = pe;
@@ -527,57 +600,57 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     }
     l_part += psum;
 
-    // O^T += V^T P^T
-    const int nv = ragged ? min(max(ctx_s - lane_tok0, 0), NZ) : NZ;  // live tokens of this lane's V fragment
-    if constexpr (FP8) {
-      for (int nn = 0; nn < 8; ++nn) {
-        const i32x4 raw = R.v[nn];
-        bf16x8 vlo = fp8x8_to_bf16(raw[0], raw[1]);
-        bf16x8 vhi = fp8x8_to_bf16(raw[2], raw[3]);
-        if (ragged) {
-          vlo = keep_first(vlo, nv);
-          vhi = keep_first(vhi, nv - 8);
-        }
-        acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vlo, p[0], acc[nn], 0, 0, 0);
-        acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vhi, p[1], acc[nn], 0, 0, 0);
-      }
-    } else {
-      for (int nn = 0; nn < 8; ++nn) {
-        bf16x8 vv = __builtin_bit_cast(bf16x8, R.v[nn]);
-        if (ragged) vv = keep_first(vv, nv);
-        acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vv, p[0], acc[nn], 0, 0, 0);
+    // O^T += V^T P^T.  A V fragment is 16 bytes: 8 bf16 tokens, or 16 fp8
+    // tokens (8 for each of two MFMAs); dead tokens are zeroed on the raw words.
+    unsigned vmask[4] = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
+    if (ragged)
+#pragma unroll
+      for (int wd = 0; wd < 4; ++wd) vmask[wd] = live_mask<FP8 ? 1 : 2>(wd, nv);
+#pragma unroll
+    for (int nn = 0; nn < 8; ++nn) {
+      i32x4 raw = R.v[nn];
+      if (ragged)
+#pragma unroll
+        for (int wd = 0; wd < 4; ++wd) raw[wd] &= (int)vmask[wd];
+      if constexpr (FP8) {
+        acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(raw[0], raw[1]), p[0], acc[nn], 0, 0, 0);
+        acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(raw[2], raw[3]), p[1], acc[nn], 0, 0, 0);
+      } else {
+        acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, raw), p[0], acc[nn], 0, 0, 0);
       }
     }
   };
 
-  // End of a piece: write the rows or a partial record.
-  auto finish_piece = [&](int ui) {
+  // End of a piece: stage its rows (whole segment) or its partial record.
+  auto finish_piece = [&](int ui) __attribute__((always_inline)) {
     const bool seg_end = cs.j == cs.nus - 1;
     if (!(seg_end || ui == n - 1)) return;
     const float l_tot = xor_sum(l_part);
     const float inv = vsc / l_tot;
     if (piece_j0 == 0 && seg_end) {  // the whole segment: final output
-      if (li < G) {
-        const size_t row = ((size_t)cs.s * a.hq + (size_t)cs.g * G + li) * kHeadDim;
-        for (int nn = 0; nn < 8; ++nn) {
-          const f32x4 o = acc[nn] * inv;
-          const size_t off = row + 16 * nn + 4 * lj;
-          if (a.out_fp32) {
-            *(f32x4*)((float*)a.out + off) = o;
-          } else {
-            u16x4 ob;
-            for (int e = 0; e < 4; ++e) ob[e] = f32_to_bf16_bits(o[e]);
-            *(u16x4*)((uint16_t*)a.out + off) = ob;
-          }
+      const int bytes = a.out_fp32 ? 8192 : 4096;
+      char* base = stg + stage_begin(bytes);
+#pragma unroll
+      for (int nn = 0; nn < 8; ++nn) {
+        const f32x4 o = acc[nn] * inv;
+        if (a.out_fp32) {
+          *(f32x4*)(base + nn * 1024 + lane * 16) = o;
+        } else {
+          u16x4 ob;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) ob[e] = f32_to_bf16_bits(o[e]);
+          *(u16x4*)(base + nn * 512 + lane * 8) = ob;
         }
       }
+      stage_meta(a.out_fp32 ? 1 : 0, (int)(base - stg), ((long long)cs.s * a.hq + (long long)cs.g * G) * kHeadDim);
     } else {  // a piece of a segment cut by slice boundaries
-      const size_t rec = (size_t)gw * 2 + (piece_first ? 0 : 1);
-      if (li < G) {
-        float* ro = a.rec_o + (rec * G + li) * kHeadDim;
-        for (int nn = 0; nn < 8; ++nn) coherent_store4(ro + 16 * nn + 4 * lj, acc[nn] * inv);
-        if (lj == 0) coherent_store2(a.rec_ml + (rec * G + li) * 2, m_run, l_tot);
-      }
+      char* base = stg + stage_begin(8192 + 512);
+#pragma unroll
+      for (int nn = 0; nn < 8; ++nn) *(f32x4*)(base + nn * 1024 + lane * 16) = acc[nn] * inv;
+      float* ml = (float*)(base + 8192 + lane * 8);
+      ml[0] = m_run;
+      ml[1] = l_tot;
+      stage_meta(2, (int)(base - stg), (long long)gw * 2 + (piece_first ? 0 : 1));
       if (piece_first) {
         arr_s0 = cs.s;
         arr_g0 = cs.g;
@@ -588,46 +661,59 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     }
   };
 
-  // One unit in flight while the previous one is computed.  The loop is
-  // unrolled by two so that both register buffers are static, and the last
-  // unit is peeled off so that every KV load inside the loop is
-  // unconditional.  Program order of the loads: Q(u+1) if u+1 starts a
-  // segment, then KV(u+1), then the computation of unit u; so waiting for a
-  // unit's query group never waits for the unit behind it.
-  Walker nx = cs;  // position of the unit after the one being computed
-  advance(nx);
+  // One unit in flight while the previous one is computed.  Per step, in
+  // program order: the K and V tiles of unit u+1; at the start of a piece,
+  // the query group of unit u's segment copied out of the ring slot of u's
+  // parity; the computation of unit u; then, only if unit u+2 starts a
+  // segment, its query group loaded into that slot.  The loop is unrolled by
+  // two so that the unit buffers and query slots are static, runs pairs of
+  // units with no exit in its body, and peels the last unit or two: with an
+  // exit inside the body, or a conditional load placed before a wait that it
+  // would join, the compiler's wait counts turn conservative and it drains
+  // every load in flight.
+  Walker w1 = cs, w2;  // positions of units u+1 and u+2
+  advance(w1);
+  w2 = w1;
+  advance(w2);
   UnitRegs RA, RB;
-  load_q(qn, cs.s, cs.g);
+  load_q(qE, cs.s, cs.g);
+  load_q(qO, w1.s, w1.g);
   issue(RA, 0);
-  auto step = [&](UnitRegs& cur, UnitRegs& nxt, int ui) {
-    begin_piece(ui);
-    if (nx.j == 0) load_q(qn, nx.s, nx.g);
+  auto step = [&](UnitRegs& cur, UnitRegs& nxt, i32x4 (&qs)[4], int ui) __attribute__((always_inline)) {
     issue(nxt, ui + 1);
+    // keep the compiler's scheduler from hoisting the computation of unit u
+    // above these loads (it would wait for unit u before issuing unit u+1)
+    __builtin_amdgcn_sched_barrier(0);
+    begin_piece(ui, qs);
+    compute_unit(cur);
+    // Unit u's operands are consumed.  If unit u+2 starts a segment, load its
+    // query group into the slot just freed: a full step passes before any
+    // wait can cover this (conditional) load.
+    if (w2.j == 0) load_q(qs, w2.s, w2.g);
+    finish_piece(ui);
+    cs = w1;
+    w1 = w2;
+    advance(w2);
+  };
+  auto last = [&](UnitRegs& cur, const i32x4 (&qs)[4], int ui) __attribute__((always_inline)) {
+    begin_piece(ui, qs);
     compute_unit(cur);
     finish_piece(ui);
-    cs = nx;
-    advance(nx);
   };
-  auto last = [&](UnitRegs& cur, int ui) {
-    begin_piece(ui);
-    compute_unit(cur);
-    finish_piece(ui);
-  };
-  // Pairs of units while at least one more unit follows the pair, then the
-  // last one or two units.  (A loop with exits in the middle of its body
-  // makes the compiler's wait-count merge at the loop header conservative,
-  // and it then drains every load in flight once per iteration.)
   int ui = 0;
   for (; ui + 2 < n; ui += 2) {
-    step(RA, RB, ui);
-    step(RB, RA, ui + 1);
+    step(RA, RB, qE, ui);
+    step(RB, RA, qO, ui + 1);
   }
-  if (ui + 1 < n) {
-    step(RA, RB, ui);
-    last(RB, ui + 1);
-  } else {
-    last(RA, ui);
+  if (ui + 1 < n) {  // two units left: the last one lands in RB; move it (and its query slot) over
+    step(RA, RB, qE, ui);
+    ++ui;
+    RA = RB;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) qE[c] = qO[c];
   }
+  last(RA, qE, ui);
+  flush();
 
   // ---- 5. signal split pieces; the last arrivers merge them ----
   if (arr_s0 >= 0 || arr_s1 >= 0) {
@@ -645,7 +731,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       const int k0 = a0 / C, kend = (a0 + nus - 1) / C;
       const int np = kend - k0 + 1;           // piece r is wave k0 + r's
       const int first_slot = 2 * k0 + (a0 > k0 * C ? 1 : 0);
-      auto piece_slot = [&](int r) { return r == 0 ? (size_t)first_slot : (size_t)2 * (k0 + r); };
+      auto piece_slot = [&](int r) __attribute__((always_inline)) { return r == 0 ? (size_t)first_slot : (size_t)2 * (k0 + r); };
       const int r = gw - k0;
       const int gfirst = r - r % kFanIn;
       const int gn = min(np, gfirst + kFanIn) - gfirst;
@@ -661,14 +747,14 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
         merge_records(a, piece_slot, np, true, s, g, 0, lane);
         continue;
       }
-      merge_records(a, [&](int i) { return piece_slot(gfirst + i); }, gn, false, s, g, (size_t)2 * TW + kg, lane);
+      merge_records(a, [&](int i) __attribute__((always_inline)) { return piece_slot(gfirst + i); }, gn, false, s, g, (size_t)2 * TW + kg, lane);
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       if (lane == 0) old = __hip_atomic_fetch_add(seg_cnt + kend, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       old = __shfl(old, 0);
       if (old != ngroups - 1) continue;
       asm volatile("" ::: "memory");
       if (lane == 0) __hip_atomic_store(seg_cnt + kend, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      auto group_slot = [&](int c) {
+      auto group_slot = [&](int c) __attribute__((always_inline)) {
         return (size_t)2 * TW + k0 + min(np, (c + 1) * kFanIn) - 1;
       };
       merge_records(a, group_slot, ngroups, true, s, g, 0, lane);
