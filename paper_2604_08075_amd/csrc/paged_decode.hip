@@ -212,10 +212,13 @@ constexpr int kFanIn = 8;
 // Log-sum-exp fold of n records, by one wave, in record order:
 // M = max_p m_p, w_p = l_p 2^(m_p - M), o = sum_p w_p o_p / sum_p w_p,
 // L = sum_p w_p.  The result goes to the output rows of segment (s, g), or
-// to record slot dst.  slot_of(i) names the i-th record's slot.
+// to record slot dst.  slot_of(i) names the i-th record's slot; record
+// own_idx (if >= 0) is this wave's own, read from its LDS staging entry
+// `own` (eight [lane] chunks of 4 floats: dims 16 nn + 4 lj .. + 4 of head
+// li at lane li + 16 lj; then each lane's (m, l)) instead of global memory.
 template <class SlotOf>
 __device__ __forceinline__ void merge_records(const DecodeArgs& a, SlotOf slot_of, int n, bool to_out, int s, int g,
-                                              size_t dst, int lane) {
+                                              size_t dst, int lane, int own_idx = -1, const char* own = nullptr) {
   const int G = a.group;
   const int npairs = G * 16;  // (head, 8-value chunk) pairs
   for (int p0 = 0; p0 < npairs; p0 += 128) {  // two pairs per lane at a time
@@ -235,7 +238,17 @@ __device__ __forceinline__ void merge_records(const DecodeArgs& a, SlotOf slot_o
       f32x4 x0[kFanIn][2], x1[kFanIn][2];
 #pragma unroll
       for (int u = 0; u < kFanIn; ++u) {
-        if (r0 + u < n) {
+        if (r0 + u == own_idx) {
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            const float* ml = (const float*)(own + 8192 + hd[i] * 8);
+            m[u][i] = ml[0];
+            l[u][i] = ml[1];
+            const int nn = d0[i] >> 4, q = (d0[i] & 15) >> 2;
+            x0[u][i] = *(const f32x4*)(own + nn * 1024 + (hd[i] + 16 * q) * 16);
+            x1[u][i] = *(const f32x4*)(own + nn * 1024 + (hd[i] + 16 * (q + 1)) * 16);
+          }
+        } else if (r0 + u < n) {
           const size_t slot = slot_of(r0 + u);
 #pragma unroll
           for (int i = 0; i < 2; ++i) {
@@ -463,8 +476,9 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   // chunk-major ([nn][lane]), then for a record each lane's (m, l).
   char* const stg = stage_lds[w];
   int st_n = 0, st_off = 0;  // entries and bytes staged (wave-uniform)
-  auto flush = [&]() __attribute__((always_inline)) {
+  auto flush = [&](int skip) __attribute__((always_inline)) {
     for (int e = 0; e < st_n; ++e) {
+      if (e == skip) continue;
       const int ko = __builtin_amdgcn_readfirstlane(stage_kind[w][e]);
       const int kind = ko & 15;
       const char* base = stg + (ko >> 4);
@@ -493,7 +507,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     st_off = 0;
   };
   auto stage_begin = [&](int bytes) __attribute__((always_inline)) {  // room for one entry; returns its LDS offset
-    if (st_n == kMaxStaged || st_off + bytes > kStageBytes) flush();
+    if (st_n == kMaxStaged || st_off + bytes > kStageBytes) flush(-1);
     const int off = st_off;
     st_off += bytes;
     return off;
@@ -515,6 +529,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   bool piece_first = true;
   // split segments this wave must signal: (s, g) of its first piece and of its last piece, s = -1 if none
   int arr_s0 = -1, arr_g0 = 0, arr_s1 = -1, arr_g1 = 0;
+  int own_entry = -1, own_x = -1;  // staging entry and arrival index of the record of the piece ending the slice
 
   auto begin_piece = [&](int ui, const i32x4 (&qs)[4]) __attribute__((always_inline)) {
     if (ui == 0 || cs.j == 0) {  // a new piece starts: its query group, fresh softmax state
@@ -650,6 +665,10 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       float* ml = (float*)(base + 8192 + lane * 8);
       ml[0] = m_run;
       ml[1] = l_tot;
+      if (ui == n - 1) {
+        own_entry = st_n;
+        own_x = piece_first ? 0 : 1;
+      }
       stage_meta(2, (int)(base - stg), (long long)gw * 2 + (piece_first ? 0 : 1));
       if (piece_first) {
         arr_s0 = cs.s;
@@ -713,51 +732,81 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     for (int c = 0; c < 4; ++c) qE[c] = qO[c];
   }
   last(RA, qE, ui);
-  flush();
 
   // ---- 5. signal split pieces; the last arrivers merge them ----
+  // Pieces are merged in groups of kFanIn consecutive pieces, then the groups.
+  // Piece r of a segment is wave k0 + r's; a group's counter and record slot
+  // belong to the wave of its last piece (whose piece is that wave's first).
+  int* const group_cnt = a.arrivals;
+  int* const seg_cnt = a.arrivals + TW;
+  struct SegInfo {
+    int k0, kend, np, first_slot, r, gfirst, gn, kg, ngroups;
+  };
+  auto seg_info = [&](int s, int g) __attribute__((always_inline)) {
+    SegInfo f;
+    const int nus = pre[s + 1] - pre[s];
+    const int a0 = Hkv * pre[s] + g * nus;  // first unit of the segment in the stream
+    f.k0 = a0 / C;
+    f.kend = (a0 + nus - 1) / C;
+    f.np = f.kend - f.k0 + 1;
+    f.first_slot = 2 * f.k0 + (a0 > f.k0 * C ? 1 : 0);
+    f.r = gw - f.k0;
+    f.gfirst = f.r - f.r % kFanIn;
+    f.gn = min(f.np, f.gfirst + kFanIn) - f.gfirst;
+    f.kg = f.k0 + f.gfirst + f.gn - 1;
+    f.ngroups = (f.np + kFanIn - 1) / kFanIn;
+    return f;
+  };
+  // The piece ending the slice is usually the last of its group to arrive
+  // (the others finished earlier in their slices).  If the group counter
+  // already shows every other piece, this wave merges with its own partial
+  // straight from LDS: no record write, no wait for it, no increment.
+  bool own_last = false;
+  SegInfo own_f = {};
+  if (own_entry >= 0) {
+    own_f = seg_info(own_x == 0 ? arr_s0 : arr_s1, own_x == 0 ? arr_g0 : arr_g1);
+    int c = 0;
+    if (lane == 0) c = __hip_atomic_load(group_cnt + own_f.kg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    own_last = __shfl(c, 0) == own_f.gn - 1;
+  }
+  flush(own_last ? own_entry : -1);
   if (arr_s0 >= 0 || arr_s1 >= 0) {
     // this wave's record stores have completed (at the coherence point)
     // before it counts them
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    int* const group_cnt = a.arrivals;
-    int* const seg_cnt = a.arrivals + TW;
+    const char* own_rec = own_entry >= 0 ? stg + (__builtin_amdgcn_readfirstlane(stage_kind[w][own_entry]) >> 4) : nullptr;
     for (int x = 0; x < 2; ++x) {
       const int s = x == 0 ? arr_s0 : arr_s1;
       if (s < 0) continue;
       const int g = x == 0 ? arr_g0 : arr_g1;
-      const int nus = pre[s + 1] - pre[s];
-      const int a0 = Hkv * pre[s] + g * nus;  // first unit of the segment in the stream
-      const int k0 = a0 / C, kend = (a0 + nus - 1) / C;
-      const int np = kend - k0 + 1;           // piece r is wave k0 + r's
-      const int first_slot = 2 * k0 + (a0 > k0 * C ? 1 : 0);
-      auto piece_slot = [&](int r) __attribute__((always_inline)) { return r == 0 ? (size_t)first_slot : (size_t)2 * (k0 + r); };
-      const int r = gw - k0;
-      const int gfirst = r - r % kFanIn;
-      const int gn = min(np, gfirst + kFanIn) - gfirst;
-      const int kg = k0 + gfirst + gn - 1;    // wave of the group's last piece
-      const int ngroups = (np + kFanIn - 1) / kFanIn;
-      int old = 0;
-      if (lane == 0) old = __hip_atomic_fetch_add(group_cnt + kg, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      old = __shfl(old, 0);
-      if (old != gn - 1) continue;  // not the group's last arrival
+      const bool mine = own_last && x == own_x;
+      const SegInfo f = mine ? own_f : seg_info(s, g);
+      auto piece_slot = [&](int r) __attribute__((always_inline)) {
+        return r == 0 ? (size_t)f.first_slot : (size_t)2 * (f.k0 + r);
+      };
+      if (!mine) {
+        int old = 0;
+        if (lane == 0) old = __hip_atomic_fetch_add(group_cnt + f.kg, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (__shfl(old, 0) != f.gn - 1) continue;  // not the group's last arrival
+      }
       asm volatile("" ::: "memory");  // record loads are issued after this branch resolves
-      if (lane == 0) __hip_atomic_store(group_cnt + kg, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (ngroups == 1) {
-        merge_records(a, piece_slot, np, true, s, g, 0, lane);
+      if (lane == 0) __hip_atomic_store(group_cnt + f.kg, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (f.ngroups == 1) {
+        merge_records(a, piece_slot, f.np, true, s, g, 0, lane, mine ? f.r : -1, own_rec);
         continue;
       }
-      merge_records(a, [&](int i) __attribute__((always_inline)) { return piece_slot(gfirst + i); }, gn, false, s, g, (size_t)2 * TW + kg, lane);
+      merge_records(a, [&](int i) __attribute__((always_inline)) { return piece_slot(f.gfirst + i); }, f.gn, false, s,
+                    g, (size_t)2 * TW + f.kg, lane, mine ? f.r - f.gfirst : -1, own_rec);
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      if (lane == 0) old = __hip_atomic_fetch_add(seg_cnt + kend, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      old = __shfl(old, 0);
-      if (old != ngroups - 1) continue;
+      int old = 0;
+      if (lane == 0) old = __hip_atomic_fetch_add(seg_cnt + f.kend, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (__shfl(old, 0) != f.ngroups - 1) continue;
       asm volatile("" ::: "memory");
-      if (lane == 0) __hip_atomic_store(seg_cnt + kend, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (lane == 0) __hip_atomic_store(seg_cnt + f.kend, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       auto group_slot = [&](int c) __attribute__((always_inline)) {
-        return (size_t)2 * TW + k0 + min(np, (c + 1) * kFanIn) - 1;
+        return (size_t)2 * TW + f.k0 + min(f.np, (c + 1) * kFanIn) - 1;
       };
-      merge_records(a, group_slot, ngroups, true, s, g, 0, lane);
+      merge_records(a, group_slot, f.ngroups, true, s, g, 0, lane);
     }
   }
 }
