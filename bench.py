@@ -9,12 +9,16 @@ of the layer's KV pool (R * KV bytes >= 1 GiB), so the 256 MB Infinity
 Cache cannot serve a step from the previous one.
 
 The headline workload is the short pool (B=128, Llama-3-70B layer shape,
-bf16 KV, C_max 8192); the long pool (B=16, C_max 65536) is reported beside
-it in the same line, as the metric compares the two.
+bf16 KV, C_max 8192); the long pool (B=16, C_max 65536), the homogeneous
+pool (B=16, mixed lengths, C_max 65536) and the Qwen3-shaped fp8 short pool
+are reported beside it in the same line, as the metric compares the pools.
+Each pool also times the KV-cache append of its batch (one new token per
+sequence), and the line carries the paper's fleet cost model evaluated with
+the decode-attention throughput ratio measured here (context only).
 
 Output: one JSON line on stdout.  Progress goes to stderr.
 
-  python bench.py [--gpus 1] [--steps 100] [--warmup 10] [--all] [--no-cpu-baseline]
+  python bench.py [--gpus 1] [--steps 100] [--warmup 10] [--configs 2,3,4,5] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -123,6 +127,32 @@ def measure(cfg: int, steps: int, warmup: int, partition_tokens: int, wgs: int):
     log(f"config {cfg}: {ms_step * 1e3:.1f} us/step, {res['gbs']:.0f} GB/s "
         f"({100 * res['gbs'] / PEAK_HBM_GBS:.1f}% of 8 TB/s), kernel {kern_ms * 1e3:.1f} us "
         f"({100 * res['kernel_gbs'] / PEAK_HBM_GBS:.1f}%), min slice {dec.partition_tokens} tokens")
+
+    # KV-cache append of one token per sequence, into the slot of each
+    # sequence's last cached token (a position that always has its block)
+    gen = torch.Generator(device="cuda").manual_seed(cfg)
+    knew = torch.randn((w.batch, w.n_kv_heads, w.head_dim), device="cuda", generator=gen).to(torch.bfloat16)
+    vnew = torch.randn((w.batch, w.n_kv_heads, w.head_dim), device="cuda", generator=gen).to(torch.bfloat16)
+    pos = (cl - 1).clamp(min=0).to(torch.int32)
+    ashape = binding.decode_shape(w.batch, w.n_q_heads, w.n_kv_heads, w.max_blocks_per_seq, w.max_context_len,
+                                  w.num_blocks, kv_fp8=fp8)
+
+    def app(i):
+        binding.kv_cache_append(knew, vnew, kl[i % layers], vl[i % layers], bt, pos, ashape, ks, vs)
+
+    for i in range(warmup):
+        app(i)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+    for i in range(steps):
+        ev[i][0].record()
+        app(i)
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    app_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / steps
+    app_bytes = w.batch * w.n_kv_heads * w.head_dim * (2 * (1 if fp8 else 2) + 2 * 2)  # cache writes + bf16 inputs
+    res["kv_append"] = {"us_per_launch": app_ms * 1e3, "bytes": app_bytes,
+                        "gbs": app_bytes / (app_ms * 1e-3) / 1e9, "tokens": w.batch}
+    log(f"config {cfg}: kv append {app_ms * 1e3:.1f} us for {w.batch} tokens x {w.n_kv_heads} heads")
     del dev
     torch.cuda.empty_cache()
     return res, w
@@ -163,8 +193,9 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=2, help="headline workload (2 = short pool)")
-    ap.add_argument("--long-config", type=int, default=3, help="long-pool workload reported beside it (0 = none)")
-    ap.add_argument("--all", action="store_true", help="also report configs 1, 4 and 5")
+    ap.add_argument("--configs", default="3,4,5",
+                    help="workloads reported beside it (3 long pool, 4 homogeneous pool, 5 Qwen3 fp8, 1 tiny)")
+    ap.add_argument("--long-config", type=int, default=None, help="only this one beside the headline (0 = none)")
     ap.add_argument("--partition-tokens", type=int, default=0)
     ap.add_argument("--wgs-per-cu", type=int, default=0, help="resident workgroups per CU (0 = library choice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -193,15 +224,14 @@ def main():
     log(f"libdpool {binding.version()} on {torch.cuda.get_device_name(0)}")
 
     head, w_head = measure(args.config, args.steps, args.warmup, args.partition_tokens, args.wgs_per_cu)
+    others = [int(c) for c in args.configs.split(",") if c.strip()] if args.long_config is None else (
+        [args.long_config] if args.long_config else [])
     extra = {}
-    if args.long_config:
-        r, _ = measure(args.long_config, args.steps, args.warmup, args.partition_tokens, args.wgs_per_cu)
-        extra["long_pool"] = r
-    if args.all:
-        for c in (1, 4, 5):
-            if c not in (args.config, args.long_config):
-                r, _ = measure(c, args.steps, args.warmup, args.partition_tokens, args.wgs_per_cu)
-                extra[f"config_{c}"] = r
+    names = {3: "long_pool", 4: "homogeneous_pool", 5: "qwen3_fp8_short_pool", 1: "tiny", 2: "short_pool"}
+    for c in others:
+        if c != args.config:
+            r, _ = measure(c, args.steps, args.warmup, args.partition_tokens, args.wgs_per_cu)
+            extra[names.get(c, f"config_{c}")] = r
 
     traffic = measured_traffic(head["name"])
     roof = {"bound": "hbm", "achieved": head["kernel_gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
@@ -216,9 +246,22 @@ def main():
                    "partition_tokens": head["partition_tokens"], "layers_rotated": head["layers_rotated"]},
         "pct_of_peak_hbm": 100.0 * head["gbs"] / PEAK_HBM_GBS,
         "seq_steps_per_s": head["seq_steps_per_s"],
+        "kv_append": head["kv_append"],
         "roofline": roof,
     }
     line.update(extra)
+    homog = extra.get("homogeneous_pool")
+    if head["name"] == "short_pool_llama70b" and homog:
+        # decode-attention throughput ratio of the short pool over the
+        # homogeneous pool (one layer, per GPU), into the Sec. 3 cost model
+        rho = head["seq_steps_per_s"] / homog["seq_steps_per_s"]
+        alpha = 0.80  # the paper's short-traffic fraction for its Azure trace at B_short = 8192
+        cm = binding.cost_model(1000.0, alpha, rho, 1.0)
+        line["cost_model"] = {
+            "rho_decode_attention": rho, "alpha": alpha, "savings_formula": cm.savings_formula,
+            "definition": "rho = (B / t_step) short pool / (B / t_step) homogeneous pool, decode attention only; "
+                          "savings = alpha (1 - 1/rho) (Sec. 3); the paper's Table 1 rho = 4.0 gives 60%",
+            "context_only": True}
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on the same workload")
         line["cpu_baseline"] = cpu_baseline(w_head)

@@ -152,6 +152,29 @@ int route_on_response(const dp_route_params* params, dp_cat_state* cats, int32_t
                       int32_t cat, int64_t req_bytes, int64_t prompt_tokens);
 
 /* ------------------------------------------------------------------------ */
+/* Fleet cost model (host only): Sec. 3, "Cost Model: Why Splitting Always  */
+/* Helps".                                                                   */
+/*   G_homo = ceil(lambda / mu_long)                                         */
+/*   G_dual = ceil(alpha * lambda / mu_short)                                */
+/*          + ceil((1 - alpha) * lambda / mu_long)                           */
+/*   rho = mu_short / mu_long;  savings_formula = alpha * (1 - 1 / rho)      */
+/*   (the boxed equation);  savings_fleet = (G_homo - G_dual) / G_homo       */
+/* lambda: request rate; alpha: fraction of traffic short; mu_*: per-GPU     */
+/* throughput of each pool, same unit as lambda.  IEEE double, in that       */
+/* order, no FMA contraction.  DP_EINVAL (nothing written) unless           */
+/* lambda > 0, 0 <= alpha <= 1 and both throughputs are positive.           */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+  int64_t g_homo;         /* GPUs of the homogeneous fleet           */
+  int64_t g_dual;         /* GPUs of the dual-pool fleet             */
+  double rho;             /* throughput gain ratio                   */
+  double savings_formula; /* alpha (1 - 1/rho)                       */
+  double savings_fleet;   /* (G_homo - G_dual) / G_homo, with ceilings */
+} dp_cost_result;
+
+int dp_cost_model(double lambda, double alpha, double mu_short, double mu_long, dp_cost_result* out);
+
+/* ------------------------------------------------------------------------ */
 /* Paged decode attention (device, asynchronous).                           */
 /*                                                                           */
 /* The per-step KV read the paper's cost model calls memory-bandwidth bound */
@@ -238,6 +261,41 @@ int paged_decode_attention(const void* q, const void* k_blocks, const void* v_bl
                            float scale, const float* k_scale, const float* v_scale,
                            void* out, const dp_decode_shape* shape, void* workspace,
                            size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* KV-cache append (device, asynchronous).                                   */
+/*                                                                           */
+/* Each decode step adds one token per sequence to the cache before the     */
+/* attention reads it (Sec. 4.4: one KV-cache lookup per layer per          */
+/* generated token); pages are 16-token blocks handed out on demand (Sec. 3 */
+/* effects 1 and 3); the FP8 deployment of Sec. 4.7 stores 8-bit floats.   */
+/* For sequence s, t = positions[s], KV head g:                             */
+/*   blk = block_tables[s][t / 16], slot = t % 16                           */
+/*   k_blocks[blk, g, slot, :] = enc(k_new[s, g, :] / k_scale[g])            */
+/*   v_blocks[blk, g, :, slot] = enc(v_new[s, g, :] / v_scale[g])            */
+/* enc() copies the bf16 bits for a bf16 cache (no scales); for an e4m3     */
+/* cache it is a correctly rounded fp32 division, clamped to +-448 and      */
+/* rounded to the nearest OCP E4M3FN value (ties to even).  Inputs are      */
+/* finite (a caller promise).                                                */
+/*                                                                           */
+/*   k_new, v_new [batch, n_kv_heads, 128] bf16, 4-byte aligned             */
+/*   k_blocks, v_blocks, block_tables: as for paged_decode_attention        */
+/*   positions    [batch] int32: the slot index of the new token; a          */
+/*                position outside [0, 16 * max_blocks_per_seq), or a block */
+/*                id outside [0, num_blocks), writes nothing for that        */
+/*                sequence                                                   */
+/*   k_scale, v_scale [n_kv_heads] fp32 (e4m3 only; NULL for bf16)          */
+/*   shape        uses batch, n_kv_heads, head_dim (128), block_size (16),   */
+/*                max_blocks_per_seq, kv_dtype, num_blocks; the other        */
+/*                fields are ignored except reserved (must be 0)            */
+/* One launch on `stream`; DP_EINVAL / DP_ENOTSUP for bad arguments (nothing */
+/* enqueued), DP_EIO if the launch fails.  Two sequences that name the same */
+/* (block, slot) race.                                                       */
+/* ------------------------------------------------------------------------ */
+int kv_cache_append(const void* k_new, const void* v_new, void* k_blocks, void* v_blocks,
+                    const int32_t* block_tables, const int32_t* positions,
+                    const float* k_scale, const float* v_scale, const dp_decode_shape* shape,
+                    void* stream);
 
 #ifdef __cplusplus
 }

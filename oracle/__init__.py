@@ -16,11 +16,13 @@ precision:
 * ``attention`` - paged decode attention (the per-step KV lookup the paper's
   cost model calls memory-bandwidth bound, Sec. 3 effect 4; 16-token
   PagedAttention blocks, Sec. 3 effect 3).
+* ``append``    - the KV-cache append of each decode step, with OCP E4M3
+  encoding for an FP8 cache (Sec. 4.4, Sec. 4.7).
 * ``pool``      - per-sequence KV bytes and concurrent-sequence count
   (Sec. 1.1, Eq. 1 and Eq. 2).
 * ``route``     - token-budget estimation, EMA calibration and pool dispatch
   (Sec. 2.1 Eq. 3-5, Sec. 2.2 Algorithm 1).
-* ``cost``      - fleet savings model (Sec. 3, boxed savings equation).
+* ``cost``      - fleet sizing and the savings model (Sec. 3, boxed equation).
 
 Parity status of each function is recorded in its module header.
 """

@@ -28,8 +28,9 @@ OUT_BF16, OUT_FP32 = 0, 1
 EXPORTS = (
     "dp_last_error", "dp_version",
     "kv_pool_create", "kv_pool_info", "kv_pool_alloc_seq", "kv_pool_free_seq", "kv_pool_destroy",
-    "route_default_params", "route_init", "route_requests", "route_on_response",
+    "route_default_params", "route_init", "route_requests", "route_on_response", "dp_cost_model",
     "paged_decode_workspace_size", "paged_decode_partition_tokens", "paged_decode_attention",
+    "kv_cache_append",
 )
 
 
@@ -57,6 +58,11 @@ class CatState(ctypes.Structure):
 
 class PoolState(ctypes.Structure):
     _fields_ = [("c_max", ctypes.c_int64), ("capacity", ctypes.c_int64), ("in_flight", ctypes.c_int64)]
+
+
+class CostResult(ctypes.Structure):
+    _fields_ = [("g_homo", ctypes.c_int64), ("g_dual", ctypes.c_int64), ("rho", ctypes.c_double),
+                ("savings_formula", ctypes.c_double), ("savings_fleet", ctypes.c_double)]
 
 
 class DecodeShape(ctypes.Structure):
@@ -94,12 +100,14 @@ def lib() -> ctypes.CDLL:
                                      ctypes.POINTER(PoolState), c_i64p, c_i32p, c_i64p, ctypes.c_int64, c_i8p, c_i64p]
         L.route_on_response.argtypes = [ctypes.POINTER(RouteParams), ctypes.POINTER(CatState), ctypes.c_int32,
                                         ctypes.c_int32, ctypes.c_int64, ctypes.c_int64]
+        L.dp_cost_model.argtypes = [ctypes.c_double] * 4 + [ctypes.POINTER(CostResult)]
         L.paged_decode_workspace_size.argtypes = [ctypes.POINTER(DecodeShape)]
         L.paged_decode_workspace_size.restype = ctypes.c_size_t
         L.paged_decode_partition_tokens.argtypes = [ctypes.POINTER(DecodeShape)]
         L.paged_decode_partition_tokens.restype = ctypes.c_int32
         L.paged_decode_attention.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_float] + [ctypes.c_void_p] * 3 + [
             ctypes.POINTER(DecodeShape), ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+        L.kv_cache_append.argtypes = [ctypes.c_void_p] * 8 + [ctypes.POINTER(DecodeShape), ctypes.c_void_p]
         _lib = L
     return _lib
 
@@ -213,6 +221,15 @@ def route_on_response(params, cats, cat: int, req_bytes: int, prompt_tokens: int
     check(lib().route_on_response(ctypes.byref(params), cats, len(cats), cat, req_bytes, prompt_tokens))
 
 
+# ---------------------------------------------------------------- cost model
+
+def cost_model(lam: float, alpha: float, mu_short: float, mu_long: float) -> CostResult:
+    """Sec. 3 fleet sizing and savings (include/dpool.h, dp_cost_model)."""
+    out = CostResult()
+    check(lib().dp_cost_model(float(lam), float(alpha), float(mu_short), float(mu_long), ctypes.byref(out)))
+    return out
+
+
 # ---------------------------------------------------------------- decode
 
 def decode_shape(batch, n_q_heads, n_kv_heads, max_blocks_per_seq, max_context_len, num_blocks, kv_fp8=False,
@@ -258,6 +275,15 @@ def paged_decode_attention(q, k_blocks, v_blocks, block_tables, context_lens, sc
         float(scale), k_scale.data_ptr() if k_scale is not None else None,
         v_scale.data_ptr() if v_scale is not None else None, out.data_ptr(), ctypes.byref(shape), ws_ptr, ws_bytes,
         _stream_ptr(stream)))
+
+
+def kv_cache_append(k_new, v_new, k_blocks, v_blocks, block_tables, positions, shape: DecodeShape, k_scale=None,
+                    v_scale=None, stream=None) -> None:
+    """Enqueue the append of one token per sequence (include/dpool.h, kv_cache_append)."""
+    check(lib().kv_cache_append(
+        k_new.data_ptr(), v_new.data_ptr(), k_blocks.data_ptr(), v_blocks.data_ptr(), block_tables.data_ptr(),
+        positions.data_ptr(), k_scale.data_ptr() if k_scale is not None else None,
+        v_scale.data_ptr() if v_scale is not None else None, ctypes.byref(shape), _stream_ptr(stream)))
 
 
 class PagedDecoder:

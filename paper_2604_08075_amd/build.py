@@ -22,8 +22,8 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libdpool.so")
 ARCH = "gfx950"
 
-HOST_SOURCES = ["status.cpp", "kv_pool.cpp", "route.cpp"]
-HIP_SOURCES = ["paged_decode.hip"]
+HOST_SOURCES = ["status.cpp", "kv_pool.cpp", "route.cpp", "cost.cpp"]
+HIP_SOURCES = ["paged_decode.hip", "kv_append.hip"]
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
              "-Wall", "-Wno-unused-function"]
