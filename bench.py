@@ -30,6 +30,8 @@ import os
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -187,6 +189,30 @@ def cpu_baseline(w, budget_s=10.0):
             "seq_steps_per_s": done_seqs / dt, "seconds": dt}
 
 
+def router_rate(binding, n=1 << 20, intervals=20000):
+    """Host-side dispatch (Algorithm 1 Route, one C call over n requests) and the
+    adaptive-threshold step, timed on this host (no GPU)."""
+    rng = np.random.default_rng(11)
+    params = binding.default_route_params()
+    cats = binding.make_categories(params, 8)
+    pools = binding.make_pools(8192, 1 << 40, 65536, 1 << 40)
+    req_bytes = (np.clip(rng.lognormal(np.log(600.0), 1.2, n), 16, 60000) * 4).astype(np.int64)
+    req_cat = rng.integers(0, 8, n).astype(np.int32)
+    req_max_out = rng.integers(16, 2048, n).astype(np.int64)
+    t0 = time.perf_counter()
+    pool_ids, _ = binding.route_requests(params, cats, pools, req_bytes, req_cat, req_max_out)
+    t_route = time.perf_counter() - t0
+    ap = binding.default_adapt_params()
+    b = 8192.0
+    t0 = time.perf_counter()
+    for i in range(intervals):
+        b, _ = binding.adapt_threshold(ap, (1000, i % 30, 0, 0), (100, (i // 7) % 5, 0, 0), b)
+    t_adapt = time.perf_counter() - t0
+    return {"route_requests_per_s": n / t_route, "requests": n, "short_fraction": float(np.mean(pool_ids == 0)),
+            "adapt_threshold_us_per_call": 1e6 * t_adapt / intervals,
+            "note": "host C calls through ctypes; the adapt figure includes the ctypes call overhead"}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -262,6 +288,7 @@ def main():
             "definition": "rho = (B / t_step) short pool / (B / t_step) homogeneous pool, decode attention only; "
                           "savings = alpha (1 - 1/rho) (Sec. 3); the paper's Table 1 rho = 4.0 gives 60%",
             "context_only": True}
+    line["router"] = router_rate(binding)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on the same workload")
         line["cpu_baseline"] = cpu_baseline(w_head)

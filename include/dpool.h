@@ -152,6 +152,49 @@ int route_on_response(const dp_route_params* params, dp_cat_state* cats, int32_t
                       int32_t cat, int64_t req_bytes, int64_t prompt_tokens);
 
 /* ------------------------------------------------------------------------ */
+/* Adaptive B_short (host only).  Sec. 7 names, as future work, a routing   */
+/* threshold that adjusts itself from preemption rate, OOM events and        */
+/* request rejections; Sec. 6 recommends alerting on a preemption rate above */
+/* 1%, and Sec. 4.6 finds any B_short in 4K-16K within 80% of peak savings.  */
+/* The paper gives no update rule; this is the library's, one call per       */
+/* control interval:                                                         */
+/*   e_i = w_preempt*preempted_i + w_oom*oom_i + w_reject*rejected_i         */
+/*   x_i = e_i / max(admitted_i, 1) - target        (i = 0 short, 1 long)    */
+/*   x_0 > 0 and x_0 > x_1:  b = b - step*b   (short pool under pressure:    */
+/*                                             send borderline traffic long) */
+/*   x_1 > 0 and x_1 > x_0:  b = b + step*b   (long pool under pressure)     */
+/*   otherwise               b unchanged                                     */
+/*   then b is clamped into [b_min, b_max].                                  */
+/* IEEE double, in exactly that order, no FMA contraction.                   */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+  int64_t admitted;  /* requests routed to the pool during the interval */
+  int64_t preempted; /* sequences preempted for want of KV cache         */
+  int64_t oom;       /* out-of-memory events                             */
+  int64_t rejected;  /* requests refused at admission                    */
+} dp_pool_signals;   /* signals[0] = short pool, signals[1] = long pool  */
+
+typedef struct {
+  double w_preempt; /* weight of a preemption (1.0)                          */
+  double w_oom;     /* weight of an OOM event (1.0)                          */
+  double w_reject;  /* weight of a rejection (1.0)                           */
+  double target;    /* tolerated events per admitted request (0.01)          */
+  double step;      /* relative change of B_short per interval (0.05)        */
+  double b_min;     /* lower bound of B_short in tokens (4096)               */
+  double b_max;     /* upper bound (16384; no use above the short C_max)     */
+} dp_adapt_params;
+
+/* Fill ap with the defaults above. */
+int route_adapt_default_params(dp_adapt_params* ap);
+
+/* One control step on *b_short (in/out).  *action (may be NULL) = -1, 0 or
+ * +1 for lowered, unchanged, raised (before the clamp).  DP_EINVAL, nothing
+ * written, unless every count is >= 0, the weights and target are >= 0,
+ * 0 < step < 1, 0 < b_min <= b_max and *b_short is finite and > 0. */
+int route_adapt_threshold(const dp_adapt_params* ap, const dp_pool_signals signals[2], double* b_short,
+                          int32_t* action);
+
+/* ------------------------------------------------------------------------ */
 /* Fleet cost model (host only): Sec. 3, "Cost Model: Why Splitting Always  */
 /* Helps".                                                                   */
 /*   G_homo = ceil(lambda / mu_long)                                         */

@@ -21,7 +21,8 @@ precision:
 * ``pool``      - per-sequence KV bytes and concurrent-sequence count
   (Sec. 1.1, Eq. 1 and Eq. 2).
 * ``route``     - token-budget estimation, EMA calibration and pool dispatch
-  (Sec. 2.1 Eq. 3-5, Sec. 2.2 Algorithm 1).
+  (Sec. 2.1 Eq. 3-5, Sec. 2.2 Algorithm 1); the adaptive threshold that
+  Sec. 7 proposes as future work (a reading of this library's own).
 * ``cost``      - fleet sizing and the savings model (Sec. 3, boxed equation).
 
 Parity status of each function is recorded in its module header.

@@ -37,6 +37,23 @@ Parity: pinned by hand-computed boundary vectors at cold start (8192 -> short,
 8193 -> long), by the closed form of n identical observations
 (c_hat_n = c + beta^n (c0 - c), sigma_n = n (1 - beta) beta^n |c0 - c|), and by
 the safety invariant (the chosen pool always has C_max >= L_total).
+
+Adaptive B_short (``adapt_threshold``).  Sec. 7 leaves as future work a
+threshold that follows runtime signals (preemption rate, OOM events,
+rejections) without manual tuning; it gives no rule.  The rule here is this
+library's reading, one step per control interval:
+  pressure_i = (w_p * preempted_i + w_o * oom_i + w_r * rejected_i) / max(admitted_i, 1)
+  excess_i   = pressure_i - target            (i = short, long)
+  short excess positive and larger  -> B_short lowered by the fraction step
+  long excess positive and larger   -> B_short raised by the fraction step
+  otherwise                         -> unchanged;  then clamped to [b_min, b_max]
+Defaults: target 0.01 (Sec. 6 alerts on a preemption rate above 1%), step
+0.05, bounds 4096..16384 (Sec. 4.6: any B_short in 4K-16K keeps over 80% of
+the peak savings), unit weights (the paper does not rank the three signals).
+Parity: the paper prints no value for it ("parity unpinned" against the paper);
+the pins are hand-computed single steps, the bounds, the dead band, and a
+closed-loop property (on a toy pool whose preemptions are its overflow, the
+controller settles within one step of the threshold that fills the pool).
 """
 from __future__ import annotations
 
@@ -126,3 +143,39 @@ def on_response(params: RouteParams, cats, cat: int, req_bytes: int, prompt_toke
     st.c_hat = params.beta * st.c_hat + one_minus_beta * c_obs
     st.sigma = params.beta * st.sigma + one_minus_beta * abs(c_obs - st.c_hat)
     return True
+
+
+@dataclass
+class AdaptParams:
+    w_preempt: float = 1.0
+    w_oom: float = 1.0
+    w_reject: float = 1.0
+    target: float = 0.01
+    step: float = 0.05
+    b_min: float = 4096.0
+    b_max: float = 16384.0
+
+
+def adapt_threshold(ap: AdaptParams, signals, b_short: float):
+    """One control step.  signals = [(admitted, preempted, oom, rejected)] * 2 (short, long).
+
+    Returns (new B_short, action) with action -1 lowered, 0 kept, +1 raised.
+    """
+    excess = []
+    for admitted, preempted, oom, rejected in signals:
+        events = ap.w_preempt * float(preempted)
+        events = events + ap.w_oom * float(oom)
+        events = events + ap.w_reject * float(rejected)
+        denom = float(admitted) if admitted > 0 else 1.0
+        excess.append(events / denom - ap.target)
+    xs, xl = excess
+    b = float(b_short)
+    action = 0
+    if xs > 0.0 and xs > xl:
+        b = b - ap.step * b
+        action = -1
+    elif xl > 0.0 and xl > xs:
+        b = b + ap.step * b
+        action = 1
+    b = min(max(b, ap.b_min), ap.b_max)
+    return b, action

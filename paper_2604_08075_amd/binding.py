@@ -28,7 +28,8 @@ OUT_BF16, OUT_FP32 = 0, 1
 EXPORTS = (
     "dp_last_error", "dp_version",
     "kv_pool_create", "kv_pool_info", "kv_pool_alloc_seq", "kv_pool_free_seq", "kv_pool_destroy",
-    "route_default_params", "route_init", "route_requests", "route_on_response", "dp_cost_model",
+    "route_default_params", "route_init", "route_requests", "route_on_response",
+    "route_adapt_default_params", "route_adapt_threshold", "dp_cost_model",
     "paged_decode_workspace_size", "paged_decode_partition_tokens", "paged_decode_attention",
     "kv_cache_append",
 )
@@ -58,6 +59,17 @@ class CatState(ctypes.Structure):
 
 class PoolState(ctypes.Structure):
     _fields_ = [("c_max", ctypes.c_int64), ("capacity", ctypes.c_int64), ("in_flight", ctypes.c_int64)]
+
+
+class PoolSignals(ctypes.Structure):
+    _fields_ = [("admitted", ctypes.c_int64), ("preempted", ctypes.c_int64), ("oom", ctypes.c_int64),
+                ("rejected", ctypes.c_int64)]
+
+
+class AdaptParams(ctypes.Structure):
+    _fields_ = [("w_preempt", ctypes.c_double), ("w_oom", ctypes.c_double), ("w_reject", ctypes.c_double),
+                ("target", ctypes.c_double), ("step", ctypes.c_double), ("b_min", ctypes.c_double),
+                ("b_max", ctypes.c_double)]
 
 
 class CostResult(ctypes.Structure):
@@ -100,6 +112,9 @@ def lib() -> ctypes.CDLL:
                                      ctypes.POINTER(PoolState), c_i64p, c_i32p, c_i64p, ctypes.c_int64, c_i8p, c_i64p]
         L.route_on_response.argtypes = [ctypes.POINTER(RouteParams), ctypes.POINTER(CatState), ctypes.c_int32,
                                         ctypes.c_int32, ctypes.c_int64, ctypes.c_int64]
+        L.route_adapt_default_params.argtypes = [ctypes.POINTER(AdaptParams)]
+        L.route_adapt_threshold.argtypes = [ctypes.POINTER(AdaptParams), ctypes.POINTER(PoolSignals),
+                                            ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int32)]
         L.dp_cost_model.argtypes = [ctypes.c_double] * 4 + [ctypes.POINTER(CostResult)]
         L.paged_decode_workspace_size.argtypes = [ctypes.POINTER(DecodeShape)]
         L.paged_decode_workspace_size.restype = ctypes.c_size_t
@@ -219,6 +234,21 @@ def route_requests(params, cats, pools, req_bytes, req_cat, req_max_out):
 
 def route_on_response(params, cats, cat: int, req_bytes: int, prompt_tokens: int) -> None:
     check(lib().route_on_response(ctypes.byref(params), cats, len(cats), cat, req_bytes, prompt_tokens))
+
+
+def default_adapt_params() -> AdaptParams:
+    p = AdaptParams()
+    check(lib().route_adapt_default_params(ctypes.byref(p)))
+    return p
+
+
+def adapt_threshold(params: AdaptParams, short_signals, long_signals, b_short: float):
+    """One control step; signals are (admitted, preempted, oom, rejected).  Returns (b_short, action)."""
+    sig = (PoolSignals * 2)(PoolSignals(*short_signals), PoolSignals(*long_signals))
+    b = ctypes.c_double(float(b_short))
+    act = ctypes.c_int32(0)
+    check(lib().route_adapt_threshold(ctypes.byref(params), sig, ctypes.byref(b), ctypes.byref(act)))
+    return b.value, act.value
 
 
 # ---------------------------------------------------------------- cost model

@@ -91,3 +91,59 @@ extern "C" int route_on_response(const dp_route_params* params, dp_cat_state* ca
   st.sigma = params->beta * st.sigma + one_minus_beta * std::fabs(c_obs - st.c_hat);  // uncertainty EMA
   return DP_OK;
 }
+
+// Adaptive B_short: the control rule include/dpool.h documents (Sec. 7's
+// future-work direction, Sec. 6's 1% preemption alert level as the default
+// target, Sec. 4.6's 4K-16K plateau as the default bounds).
+extern "C" int route_adapt_default_params(dp_adapt_params* ap) {
+  if (!ap) return dpool::fail(DP_EINVAL, "route_adapt_default_params: null");
+  ap->w_preempt = 1.0;
+  ap->w_oom = 1.0;
+  ap->w_reject = 1.0;
+  ap->target = 0.01;
+  ap->step = 0.05;
+  ap->b_min = 4096.0;
+  ap->b_max = 16384.0;
+  return DP_OK;
+}
+
+extern "C" int route_adapt_threshold(const dp_adapt_params* ap, const dp_pool_signals signals[2], double* b_short,
+                                     int32_t* action) {
+  using dpool::fail;
+  if (!ap || !signals || !b_short) return fail(DP_EINVAL, "route_adapt_threshold: null argument");
+  for (int i = 0; i < 2; ++i) {
+    const dp_pool_signals& g = signals[i];
+    if (g.admitted < 0 || g.preempted < 0 || g.oom < 0 || g.rejected < 0)
+      return fail(DP_EINVAL, "route_adapt_threshold: negative count in pool %d", i);
+  }
+  if (!(ap->w_preempt >= 0.0 && ap->w_oom >= 0.0 && ap->w_reject >= 0.0 && ap->target >= 0.0))
+    return fail(DP_EINVAL, "route_adapt_threshold: weights and target must be >= 0");
+  if (!(ap->step > 0.0 && ap->step < 1.0)) return fail(DP_EINVAL, "route_adapt_threshold: step must be in (0, 1)");
+  if (!(ap->b_min > 0.0 && ap->b_min <= ap->b_max && std::isfinite(ap->b_max)))
+    return fail(DP_EINVAL, "route_adapt_threshold: need 0 < b_min <= b_max < inf");
+  const double b = *b_short;
+  if (!(std::isfinite(b) && b > 0.0)) return fail(DP_EINVAL, "route_adapt_threshold: b_short must be finite and > 0");
+  double x[2];
+  for (int i = 0; i < 2; ++i) {
+    const dp_pool_signals& g = signals[i];
+    double e = ap->w_preempt * (double)g.preempted;
+    e = e + ap->w_oom * (double)g.oom;
+    e = e + ap->w_reject * (double)g.rejected;
+    const double n = g.admitted > 0 ? (double)g.admitted : 1.0;
+    x[i] = e / n - ap->target;
+  }
+  double nb = b;
+  int32_t act = 0;
+  if (x[kShort] > 0.0 && x[kShort] > x[kLong]) {
+    nb = b - ap->step * b;
+    act = -1;
+  } else if (x[kLong] > 0.0 && x[kLong] > x[kShort]) {
+    nb = b + ap->step * b;
+    act = 1;
+  }
+  if (nb < ap->b_min) nb = ap->b_min;
+  if (nb > ap->b_max) nb = ap->b_max;
+  *b_short = nb;
+  if (action) *action = act;
+  return DP_OK;
+}
