@@ -16,6 +16,8 @@ precision:
 * ``attention`` - paged decode attention (the per-step KV lookup the paper's
   cost model calls memory-bandwidth bound, Sec. 3 effect 4; 16-token
   PagedAttention blocks, Sec. 3 effect 3).
+* ``prefill``   - causal chunked-prefill attention over the same paged cache
+  (Sec. 1.2: each pool runs chunked prefill internally).
 * ``append``    - the KV-cache append of each decode step, with OCP E4M3
   encoding for an FP8 cache (Sec. 4.4, Sec. 4.7).
 * ``pool``      - per-sequence KV bytes and concurrent-sequence count
