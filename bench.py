@@ -189,6 +189,64 @@ def cpu_baseline(w, budget_s=10.0):
             "seq_steps_per_s": done_seqs / dt, "seconds": dt}
 
 
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA peak
+
+
+def prefill_flops(w) -> int:
+    """Algorithmic flops of causal chunked-prefill attention: 4 * D * Hq per attended (query, token) pair."""
+    qs = w.meta["q_start"]
+    pairs = 0
+    for s in range(w.batch):
+        n, T = int(qs[s + 1] - qs[s]), int(w.context_lens[s])
+        pairs += n * (T - n) + n * (n + 1) // 2
+    return 4 * w.head_dim * w.n_q_heads * pairs
+
+
+def measure_prefill(name, steps, warmup, query_tile=0):
+    """Time chunked_prefill_attention on one of the prefill workloads (HIP events, current stream)."""
+    import torch
+
+    import workloads
+    from paper_2604_08075_amd import binding
+    w = workloads.make_prefill_config(name, poison=False)
+    dev = workloads.to_device(w, poison_unused=False)
+    fp8 = w.kv_format == "fp8_e4m3"
+    total_q = int(w.meta["q_start"][-1])
+    shape = binding.prefill_shape(w.batch, w.n_q_heads, w.n_kv_heads, w.max_blocks_per_seq, w.max_context_len,
+                                  w.num_blocks, total_q, kv_fp8=fp8, query_tile=query_tile)
+    out = torch.empty((total_q, w.n_q_heads, w.head_dim), dtype=torch.bfloat16, device="cuda")
+
+    def call():
+        binding.chunked_prefill_attention(dev["q"], dev["k"][0], dev["v"][0], dev["block_tables"],
+                                          dev["context_lens"], dev["q_start"], w.scale, out, shape, dev["k_scale"],
+                                          dev["v_scale"])
+
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    flops = prefill_flops(w)
+    tfs = flops / (ms * 1e-3) / 1e12
+    chunks = ", ".join(f"{int(w.meta['q_start'][s + 1] - w.meta['q_start'][s])}@{int(w.context_lens[s])}"
+                       for s in range(w.batch))
+    log(f"prefill {name}: {ms * 1e3:.1f} us/launch, {tfs:.1f} TFLOP/s ({100 * tfs / PEAK_BF16_TFLOPS:.1f}% of "
+        f"bf16 MFMA peak)")
+    del dev
+    torch.cuda.empty_cache()
+    return {"workload": f"{name}: chunks (query tokens @ context) {chunks}, {w.n_q_heads}q/{w.n_kv_heads}kv, "
+                        f"head_dim 128, {w.kv_format} KV, block 16",
+            "us_per_launch": ms * 1e3, "flops": flops, "tflops": tfs,
+            "roofline": {"bound": "mfma", "achieved": tfs, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                         "frac": tfs / PEAK_BF16_TFLOPS, "kernel": "prefill_kernel"},
+            "query_tile": query_tile or 64}
+
+
 def router_rate(binding, n=1 << 20, intervals=20000):
     """Host-side dispatch (Algorithm 1 Route, one C call over n requests) and the
     adaptive-threshold step, timed on this host (no GPU)."""
@@ -225,6 +283,9 @@ def main():
     ap.add_argument("--partition-tokens", type=int, default=0)
     ap.add_argument("--wgs-per-cu", type=int, default=0, help="resident workgroups per CU (0 = library choice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-prefill", action="store_true", help="skip the chunked-prefill attention timing")
+    ap.add_argument("--prefill-tile", type=int, default=0, help="query tokens per prefill workgroup (32/64)")
+    ap.add_argument("--prefill-only", action="store_true", help="only time the chunked-prefill attention")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB 10 times (counter calibration) and exit")
     args = ap.parse_args()
@@ -249,6 +310,11 @@ def main():
     from paper_2604_08075_amd import binding
     log(f"libdpool {binding.version()} on {torch.cuda.get_device_name(0)}")
 
+    if args.prefill_only:
+        res = {n: measure_prefill(n, max(args.steps // 5, 5), 3, args.prefill_tile)
+               for n in ("chunked_prefill_llama70b", "chunked_prefill_qwen3_fp8")}
+        print(json.dumps({"chunked_prefill": res}), flush=True)
+        return
     head, w_head = measure(args.config, args.steps, args.warmup, args.partition_tokens, args.wgs_per_cu)
     others = [int(c) for c in args.configs.split(",") if c.strip()] if args.long_config is None else (
         [args.long_config] if args.long_config else [])
@@ -289,6 +355,9 @@ def main():
                           "savings = alpha (1 - 1/rho) (Sec. 3); the paper's Table 1 rho = 4.0 gives 60%",
             "context_only": True}
     line["router"] = router_rate(binding)
+    if not args.no_prefill:
+        line["chunked_prefill"] = {n: measure_prefill(n, max(args.steps // 5, 5), 3, args.prefill_tile)
+                                   for n in ("chunked_prefill_llama70b", "chunked_prefill_qwen3_fp8")}
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on the same workload")
         line["cpu_baseline"] = cpu_baseline(w_head)

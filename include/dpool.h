@@ -340,6 +340,56 @@ int kv_cache_append(const void* k_new, const void* v_new, void* k_blocks, void* 
                     const float* k_scale, const float* v_scale, const dp_decode_shape* shape,
                     void* stream);
 
+/* ------------------------------------------------------------------------ */
+/* Chunked-prefill attention (device, asynchronous).                        */
+/*                                                                           */
+/* Each pool runs chunked prefill internally (Sec. 1.2): a prompt is        */
+/* attended in chunks (2,048 tokens by default) whose K and V are already   */
+/* in the paged cache (kv_cache_append, or any writer of the same layout).  */
+/* For sequence s with T = context_lens[s] cached tokens (the chunk         */
+/* included) and n = q_start[s+1] - q_start[s] query rows, row              */
+/* r = q_start[s] + i sits at position p = T - n + i and, for query head h  */
+/* (KV head g = h / G):                                                      */
+/*   out[r,h,:] = sum_{t <= p} softmax_t(scale * q[r,h,:] . K_t) V_t         */
+/* with K_t, V_t gathered exactly as for paged_decode_attention.  Decode is */
+/* the case n = 1.                                                           */
+/*                                                                           */
+/* Layouts: q and out [total_q, n_q_heads, 128] (bf16 / out_dtype), rows    */
+/* packed sequence after sequence as q_start says; k_blocks, v_blocks,      */
+/* block_tables, context_lens, k_scale, v_scale as for decode; q_start      */
+/* [batch + 1] int32 on the device, non-decreasing, q_start[0] = 0,         */
+/* q_start[batch] <= total_q.  A caller promise: n <= T for every sequence. */
+/* Values that break it (or q_start out of order) are clamped: no access    */
+/* leaves the buffers, rows past min(n, T) are left unwritten and rows of   */
+/* overlapping ranges are unspecified.  No workspace; nothing is allocated. */
+/* Supported: head_dim 128, block_size 16, Hq a multiple of Hkv,            */
+/* batch <= 4096.                                                            */
+/* ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t batch;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t block_size;
+  int32_t max_blocks_per_seq;
+  int32_t max_context_len;
+  int32_t kv_dtype;   /* DP_KV_*                                             */
+  int32_t out_dtype;  /* DP_OUT_*                                            */
+  int32_t query_tile; /* query tokens per workgroup: 32 or 64; 0 = library's */
+  int32_t reserved;   /* must be 0                                           */
+  int64_t total_q;    /* rows of q and out                                   */
+  int64_t num_blocks; /* blocks in k_blocks / v_blocks                       */
+} dp_prefill_shape;
+
+/* Enqueue the chunked-prefill attention on `stream` as one kernel launch.
+ * Host-side validation as for decode (DP_EINVAL / DP_ENOTSUP, nothing
+ * enqueued); DP_EIO if the launch fails. */
+int chunked_prefill_attention(const void* q, const void* k_blocks, const void* v_blocks,
+                              const int32_t* block_tables, const int32_t* context_lens,
+                              const int32_t* q_start, float scale, const float* k_scale,
+                              const float* v_scale, void* out, const dp_prefill_shape* shape,
+                              void* stream);
+
 #ifdef __cplusplus
 }
 #endif

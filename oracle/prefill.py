@@ -42,13 +42,16 @@ from .attention import _gather_rows
 
 
 def chunked_prefill_attention(q_bits, k_pool, v_pool, block_tables, context_lens, q_start, scale,
-                              kv_format="bf16", k_scale=None, v_scale=None, block_size=16, seqs=None):
-    """float64 [total_q, Hq, D] (rows of sequences not in ``seqs`` are left NaN).
+                              kv_format="bf16", k_scale=None, v_scale=None, block_size=16, seqs=None, rows=None):
+    """float64 [total_q, Hq, D] (rows not computed are left NaN).
 
     q_bits  : uint16 [total_q, Hq, D] bf16 codes, sequences packed by q_start
     q_start : int [B + 1], non-decreasing, q_start[0] = 0, q_start[B] = total_q
+    seqs    : optional sequences to compute; rows: optional global row indices
+              to compute (a sample; each row is computed exactly as in full)
     other arguments as for attention.paged_decode_attention
     """
+    want = None if rows is None else set(int(r) for r in rows)
     q = numerics.decode_bf16(q_bits)
     total_q, Hq, D = q.shape
     q_start = np.asarray(q_start, dtype=np.int64)
@@ -66,15 +69,18 @@ def chunked_prefill_attention(q_bits, k_pool, v_pool, block_tables, context_lens
             continue
         if n > T:
             raise ValueError(f"sequence {s}: {n} query tokens but only {T} cached tokens")
-        pos = T - n + np.arange(n)                       # absolute position of each query row
-        future = np.arange(T)[None, :] > pos[:, None]    # [n, T]: token after the query
+        sel = np.arange(r0, r1) if want is None else np.array(sorted(r for r in want if r0 <= r < r1), np.int64)
+        if len(sel) == 0:
+            continue
+        pos = T - n + (sel - r0)                         # absolute position of each query row
+        future = np.arange(T)[None, :] > pos[:, None]    # [rows, T]: token after the query
         bt = np.asarray(block_tables[s])
         for g in range(Hkv):
             K = ks[g] * numerics.decode(_gather_rows(k_pool, bt, g, T, block_size, False), kv_format)
             V = vs[g] * numerics.decode(_gather_rows(v_pool, bt, g, T, block_size, True), kv_format)
             for h in range(g * G, (g + 1) * G):
-                z = scale * (q[r0:r1, h] @ K.T)           # [n, T]
+                z = scale * (q[sel, h] @ K.T)             # [rows, T]
                 z[future] = -np.inf
                 w = np.exp(z - z.max(axis=1, keepdims=True))
-                out[r0:r1, h] = (w @ V) / w.sum(axis=1, keepdims=True)
+                out[sel, h] = (w @ V) / w.sum(axis=1, keepdims=True)
     return out

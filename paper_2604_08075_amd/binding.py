@@ -31,7 +31,7 @@ EXPORTS = (
     "route_default_params", "route_init", "route_requests", "route_on_response",
     "route_adapt_default_params", "route_adapt_threshold", "dp_cost_model",
     "paged_decode_workspace_size", "paged_decode_partition_tokens", "paged_decode_attention",
-    "kv_cache_append",
+    "kv_cache_append", "chunked_prefill_attention",
 )
 
 
@@ -86,6 +86,14 @@ class DecodeShape(ctypes.Structure):
                 ("reserved", ctypes.c_int32), ("num_blocks", ctypes.c_int64)]
 
 
+class PrefillShape(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("block_size", ctypes.c_int32),
+                ("max_blocks_per_seq", ctypes.c_int32), ("max_context_len", ctypes.c_int32),
+                ("kv_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32), ("query_tile", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("total_q", ctypes.c_int64), ("num_blocks", ctypes.c_int64)]
+
+
 _lib = None
 
 
@@ -123,6 +131,8 @@ def lib() -> ctypes.CDLL:
         L.paged_decode_attention.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_float] + [ctypes.c_void_p] * 3 + [
             ctypes.POINTER(DecodeShape), ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
         L.kv_cache_append.argtypes = [ctypes.c_void_p] * 8 + [ctypes.POINTER(DecodeShape), ctypes.c_void_p]
+        L.chunked_prefill_attention.argtypes = [ctypes.c_void_p] * 6 + [ctypes.c_float] + [ctypes.c_void_p] * 3 + [
+            ctypes.POINTER(PrefillShape), ctypes.c_void_p]
         _lib = L
     return _lib
 
@@ -314,6 +324,23 @@ def kv_cache_append(k_new, v_new, k_blocks, v_blocks, block_tables, positions, s
         k_new.data_ptr(), v_new.data_ptr(), k_blocks.data_ptr(), v_blocks.data_ptr(), block_tables.data_ptr(),
         positions.data_ptr(), k_scale.data_ptr() if k_scale is not None else None,
         v_scale.data_ptr() if v_scale is not None else None, ctypes.byref(shape), _stream_ptr(stream)))
+
+
+def prefill_shape(batch, n_q_heads, n_kv_heads, max_blocks_per_seq, max_context_len, num_blocks, total_q,
+                  kv_fp8=False, out_fp32=False, query_tile=0, head_dim=128, block_size=16) -> PrefillShape:
+    return PrefillShape(batch, n_q_heads, n_kv_heads, head_dim, block_size, max_blocks_per_seq, max_context_len,
+                        KV_FP8_E4M3 if kv_fp8 else KV_BF16, OUT_FP32 if out_fp32 else OUT_BF16, query_tile, 0,
+                        total_q, num_blocks)
+
+
+def chunked_prefill_attention(q, k_blocks, v_blocks, block_tables, context_lens, q_start, scale, out,
+                              shape: PrefillShape, k_scale=None, v_scale=None, stream=None) -> None:
+    """Enqueue the chunked-prefill attention (include/dpool.h, chunked_prefill_attention)."""
+    check(lib().chunked_prefill_attention(
+        q.data_ptr(), k_blocks.data_ptr(), v_blocks.data_ptr(), block_tables.data_ptr(), context_lens.data_ptr(),
+        q_start.data_ptr(), float(scale), k_scale.data_ptr() if k_scale is not None else None,
+        v_scale.data_ptr() if v_scale is not None else None, out.data_ptr(), ctypes.byref(shape),
+        _stream_ptr(stream)))
 
 
 class PagedDecoder:

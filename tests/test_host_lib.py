@@ -276,3 +276,44 @@ def test_decoder_wrapper_constructs_on_host(host_lib):
     assert tuple(dec.new_out("cpu").shape) == (4, 8, 128)
     with pytest.raises(host_lib.DpoolError):
         host_lib.PagedDecoder(4, 8, 2, 64, 1000, 300, partition_tokens=24, device="cpu")
+
+
+# ---------------------------------------------------------------- chunked prefill (host-side validation only)
+
+def pshape(host_lib, **kw):
+    args = dict(batch=4, n_q_heads=8, n_kv_heads=2, max_blocks_per_seq=64, max_context_len=1000, num_blocks=300,
+                total_q=100)
+    args.update({k: kw.pop(k) for k in list(kw) if k in args})
+    s = host_lib.prefill_shape(**args, **{k: v for k, v in kw.items() if k in ("kv_fp8", "out_fp32", "query_tile")})
+    for k, v in kw.items():
+        if k not in ("kv_fp8", "out_fp32", "query_tile"):
+            setattr(s, k, v)
+    return s
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(head_dim=64), -95), (dict(block_size=32), -95), (dict(n_q_heads=12, n_kv_heads=8), -22),
+    (dict(max_context_len=64 * 16 + 1), -22), (dict(query_tile=48), -22), (dict(num_blocks=0), -22),
+    (dict(batch=-1), -22), (dict(batch=5000), -95), (dict(total_q=-1), -22), (dict(reserved=1), -22),
+    (dict(kv_dtype=2), -95), (dict(out_dtype=3), -95),
+])
+def test_prefill_invalid_shapes_rejected_on_host(host_lib, kw, code):
+    s = pshape(host_lib, **kw)
+    L = host_lib.lib()
+    assert L.chunked_prefill_attention(16, 16, 16, 16, 16, 16, 1.0, None, None, 16, ctypes.byref(s), None) == code
+    assert host_lib.last_error() != ""
+
+
+def test_prefill_bad_pointers_and_scale_rejected_on_host(host_lib):
+    L = host_lib.lib()
+    s = pshape(host_lib)
+    assert L.chunked_prefill_attention(None, 16, 16, 16, 16, 16, 1.0, None, None, 16, ctypes.byref(s), None) == -22
+    assert L.chunked_prefill_attention(8, 16, 16, 16, 16, 16, 1.0, None, None, 16, ctypes.byref(s), None) == -22
+    assert L.chunked_prefill_attention(16, 16, 16, 16, 16, 16, 1.0, 16, 16, 16, ctypes.byref(s), None) == -22
+    sf = pshape(host_lib, kv_fp8=True)
+    assert L.chunked_prefill_attention(16, 16, 16, 16, 16, 16, 1.0, None, None, 16, ctypes.byref(sf), None) == -22
+    for bad in (0.0, -1.0, float("nan"), float("inf")):
+        assert L.chunked_prefill_attention(16, 16, 16, 16, 16, 16, bad, None, None, 16, ctypes.byref(s), None) == -22
+    empty = pshape(host_lib, total_q=0)
+    assert L.chunked_prefill_attention(None, None, None, None, None, None, 1.0, None, None, None,
+                                       ctypes.byref(empty), None) == 0   # nothing to do, nothing enqueued

@@ -141,3 +141,14 @@ def test_more_queries_than_cached_tokens_is_rejected():
     qb, kb, vb, bt, ctx, q_start = prefill_case(rng, 4, 2, [10], [10])
     with pytest.raises(ValueError):
         run(qb, kb, vb, bt, np.array([9]), q_start)
+
+
+def test_sampled_rows_equal_full_rows():
+    rng = np.random.default_rng(9)
+    case = prefill_case(rng, 8, 2, [200, 90], [120, 90])
+    full = run(*case)
+    rows = [0, 5, 119, 120, 150, 209]
+    got = run(*case, rows=rows)
+    np.testing.assert_allclose(got[rows], full[rows], rtol=1e-12, atol=1e-15)   # BLAS blocking may differ
+    others = np.setdiff1d(np.arange(210), rows)
+    assert np.isnan(got[others]).all()

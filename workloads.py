@@ -245,6 +245,43 @@ def make_config(i: int, seed: int | None = None, poison: bool = True) -> Workloa
                          name=c["name"], rng=rng)
 
 
+# Chunked-prefill workloads: each sequence's chunk is the last n tokens of its
+# context (its K and V already cached).  name -> (heads, KV format, C_max, pool
+# blocks, [(chunk tokens n, context tokens T)]).  The 2,048-token chunk is
+# vLLM's default chunk size (Sec. 1.2); the contexts place one chunk at the
+# start of a prompt and others deep into long prompts of the long pool.
+PREFILL_CONFIGS = {
+    "chunked_prefill_llama70b": dict(n_q_heads=64, n_kv_heads=8, kv="bf16", c_max=65536, num_blocks=49152,
+                                     chunks=[(2048, 2048), (2048, 8192), (2048, 16384), (2048, 32768)]),
+    "chunked_prefill_qwen3_fp8": dict(n_q_heads=64, n_kv_heads=4, kv="fp8_e4m3", c_max=8192, num_blocks=167936,
+                                      chunks=[(2048, 2048), (2048, 4096), (2048, 6144), (2048, 8192)]),
+}
+
+
+def make_prefill(chunks, n_q_heads, n_kv_heads, c_max, kv_format="bf16", num_blocks=None, seed=0,
+                 poison=True, name="custom_prefill") -> Workload:
+    """A workload whose q_bits are the packed chunk queries [total_q, Hq, D] and whose
+    meta["q_start"] holds the row offsets [B + 1]; contexts and KV as make_workload draws
+    them (same generator, the chunk queries drawn after V)."""
+    chunks = [(int(n), int(t)) for n, t in chunks]
+    if any(n > t or n < 0 for n, t in chunks):
+        raise ValueError("each chunk needs 0 <= n <= T")
+    rng = np.random.default_rng(seed)
+    w = make_workload(len(chunks), n_q_heads, n_kv_heads, [t for _, t in chunks], c_max, kv_format,
+                      num_blocks=num_blocks, seed=seed, poison=poison, name=name, rng=rng)
+    q_start = np.concatenate([[0], np.cumsum([n for n, _ in chunks])]).astype(np.int32)
+    q = rng.standard_normal((int(q_start[-1]), n_q_heads, HEAD_DIM), dtype=np.float32)
+    w.q_bits = to_bf16_codes(q)
+    w.meta["q_start"] = q_start
+    return w
+
+
+def make_prefill_config(name: str, seed: int = 7, poison: bool = True) -> Workload:
+    c = PREFILL_CONFIGS[name]
+    return make_prefill(c["chunks"], c["n_q_heads"], c["n_kv_heads"], c["c_max"], c["kv"], c["num_blocks"],
+                        seed=seed, poison=poison, name=name)
+
+
 def to_device(w: Workload, device="cuda", layers: int = 1, poison_unused: bool = True):
     """Place a workload in device memory (torch tensors; plumbing only).
 
@@ -272,6 +309,8 @@ def to_device(w: Workload, device="cuda", layers: int = 1, poison_unused: bool =
     out["q"] = torch.from_numpy(w.q_bits.view(np.int16)).to(device)
     out["block_tables"] = torch.from_numpy(w.block_tables).to(device)
     out["context_lens"] = torch.from_numpy(w.context_lens).to(device)
+    if "q_start" in w.meta:
+        out["q_start"] = torch.from_numpy(w.meta["q_start"]).to(device)
     out["k_scale"] = torch.from_numpy(w.k_scale).to(device) if fp8 else None
     out["v_scale"] = torch.from_numpy(w.v_scale).to(device) if fp8 else None
     return out
