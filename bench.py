@@ -244,7 +244,7 @@ def measure_prefill(name, steps, warmup, query_tile=0):
             "us_per_launch": ms * 1e3, "flops": flops, "tflops": tfs,
             "roofline": {"bound": "mfma", "achieved": tfs, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                          "frac": tfs / PEAK_BF16_TFLOPS, "kernel": "prefill_kernel"},
-            "query_tile": query_tile or 64}
+            "query_tile": query_tile or 32}
 
 
 def router_rate(binding, n=1 << 20, intervals=20000):

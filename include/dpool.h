@@ -363,7 +363,7 @@ int kv_cache_append(const void* k_new, const void* v_new, void* k_blocks, void* 
 /* leaves the buffers, rows past min(n, T) are left unwritten and rows of   */
 /* overlapping ranges are unspecified.  No workspace; nothing is allocated. */
 /* Supported: head_dim 128, block_size 16, Hq a multiple of Hkv,            */
-/* batch <= 4096.                                                            */
+/* batch <= 4096, max_context_len <= 65536 (the long pool's C_max).          */
 /* ------------------------------------------------------------------------ */
 typedef struct {
   int32_t batch;

@@ -57,6 +57,7 @@ constexpr int kKStage = kKT * kKRow;  // bf16 per K stage
 constexpr int kVStage = kD * kVRow;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kMaxBatch = 4096;
+constexpr int kIdCap = 4096;          // block ids staged in LDS: contexts up to 65,536 tokens
 
 struct PrefillArgs {
   const uint16_t* q;            // [total_q, Hq, 128] bf16
@@ -74,13 +75,16 @@ struct PrefillArgs {
   int32_t total_q;
 };
 
+// Max over the four lanes li, li + 16, li + 32, li + 48: the permlane swaps
+// pair each lane's value with its partner 16 (then 32) lanes away without a
+// trip through LDS.
 __device__ __forceinline__ float xor_max(float x) {
-  x = fmaxf(x, __shfl_xor(x, 16));
-  return fmaxf(x, __shfl_xor(x, 32));
-}
-__device__ __forceinline__ float xor_sum(float x) {
-  x += __shfl_xor(x, 16);
-  return x + __shfl_xor(x, 32);
+  const unsigned u = __builtin_bit_cast(unsigned, x);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  x = fmaxf(__builtin_bit_cast(float, (unsigned)a[0]), __builtin_bit_cast(float, (unsigned)a[1]));
+  const unsigned v = __builtin_bit_cast(unsigned, x);
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return fmaxf(__builtin_bit_cast(float, (unsigned)b[0]), __builtin_bit_cast(float, (unsigned)b[1]));
 }
 
 // Eight e4m3 bytes -> eight bf16 (exact).
@@ -109,10 +113,11 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float x) { return __builtin
 
 // R: 16-token query column blocks per wave, so QT = 16 R query tokens per workgroup.
 template <bool FP8, int R>
-__global__ __launch_bounds__(kWaves * 64) void prefill_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(kWaves * 64, R == 2 ? 2 : 1) void prefill_kernel(PrefillArgs a) {
   constexpr int QT = 16 * R;
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][kKStage];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][kVStage];
+  __shared__ int ids_lds[kIdCap];    // the sequence's block ids, clamped into the pool
   extern __shared__ int tile_pre[];  // [B + 1] query tiles of sequences 0..s-1
 
   const int tid = threadIdx.x;
@@ -206,15 +211,21 @@ __global__ __launch_bounds__(kWaves * 64) void prefill_kernel(PrefillArgs a) {
 
   // ---- cooperative tile copy: cache -> registers -> LDS ----
   constexpr int NCH = FP8 ? 1 : 2;  // 16-byte chunks per thread, each of K and V
-  i32x4 kreg[NCH], vreg[NCH];
+  // Block ids come from LDS, staged once: a block-table load inside the loop
+  // would sit behind the tile loads on the in-order memory counter, and
+  // waiting for it would drain the tile prefetch.
+  const int n_ids = min(min(2 * ntile, nb), kIdCap);
+  for (int i = tid; i < n_ids; i += kWaves * 64) {
+    const int id = bt[i];
+    ids_lds[i] = id < 0 ? 0 : (id > a.num_blocks_m1 ? a.num_blocks_m1 : id);
+  }
+  __syncthreads();
   auto block_id = [&](int j, int b) __attribute__((always_inline)) {
     int bi = 2 * j + b;
     if (bi >= nb) bi = 2 * j;  // a block past the sequence re-reads the tile's first (then zeroed / masked)
-    int id = bt[bi];
-    id = id < 0 ? 0 : (id > a.num_blocks_m1 ? a.num_blocks_m1 : id);
-    return (size_t)id * a.hkv + g;
+    return (size_t)ids_lds[bi] * a.hkv + g;
   };
-  auto load_tile = [&](int j) __attribute__((always_inline)) {
+  auto load_tile = [&](int j, i32x4 (&kreg)[NCH], i32x4 (&vreg)[NCH]) __attribute__((always_inline)) {
     if constexpr (FP8) {
       const int b = tid >> 7, x = tid & 127;
       const size_t tile = block_id(j, b);
@@ -230,7 +241,8 @@ __global__ __launch_bounds__(kWaves * 64) void prefill_kernel(PrefillArgs a) {
       }
     }
   };
-  auto store_tile = [&](int j, int buf) __attribute__((always_inline)) {
+  auto store_tile = [&](int j, int buf, const i32x4 (&kreg)[NCH], const i32x4 (&vreg)[NCH])
+                        __attribute__((always_inline)) {
     uint16_t* kl = k_lds[buf];
     uint16_t* vl = v_lds[buf];
     const int t0 = kKT * j;
@@ -242,15 +254,20 @@ __global__ __launch_bounds__(kWaves * 64) void prefill_kernel(PrefillArgs a) {
       *(i32x4*)(kd + 8) = fp8x8_to_bf16(kreg[0][2], kreg[0][3]);
       // V: dim x, tokens 16b .. +16
       uint16_t* vd = vl + x * kVRow + 16 * b;
-      *(i32x4*)vd = zero_tokens_from(fp8x8_to_bf16(vreg[0][0], vreg[0][1]), t0 + 16 * b, T);
-      *(i32x4*)(vd + 8) = zero_tokens_from(fp8x8_to_bf16(vreg[0][2], vreg[0][3]), t0 + 16 * b + 8, T);
+      i32x4 v0 = fp8x8_to_bf16(vreg[0][0], vreg[0][1]), v1 = fp8x8_to_bf16(vreg[0][2], vreg[0][3]);
+      if (t0 + kKT > T) {  // the sequence ends inside this tile
+        v0 = zero_tokens_from(v0, t0 + 16 * b, T);
+        v1 = zero_tokens_from(v1, t0 + 16 * b + 8, T);
+      }
+      *(i32x4*)vd = v0;
+      *(i32x4*)(vd + 8) = v1;
     } else {
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         const int c = tid + 256 * i, b = c >> 8, x = c & 255;
         *(i32x4*)(kl + (16 * b + (x >> 4)) * kKRow + 8 * (x & 15)) = kreg[i];
         const int first = 16 * b + 8 * (x & 1);
-        *(i32x4*)(vl + (x >> 1) * kVRow + first) = zero_tokens_from(vreg[i], t0 + first, T);
+        *(i32x4*)(vl + (x >> 1) * kVRow + first) = t0 + kKT > T ? zero_tokens_from(vreg[i], t0 + first, T) : vreg[i];
       }
     }
   };
@@ -264,23 +281,26 @@ __global__ __launch_bounds__(kWaves * 64) void prefill_kernel(PrefillArgs a) {
   const int voff = li * kVRow + 8 * lj;  // + 16 nn rows
 
   f32x4 acc[R][8];
-  float m_run[R], l_part[R];
+  float m_run[R];
+  f32x4 lsum[R];  // column sums of P, accumulated by the matrix cores (every row holds the sum)
 #pragma unroll
   for (int rb = 0; rb < R; ++rb) {
     m_run[rb] = -INFINITY;
-    l_part[rb] = 0.f;
+    lsum[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int nn = 0; nn < 8; ++nn) acc[rb][nn] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  load_tile(0);
-  store_tile(0, 0);
-  __syncthreads();
-  for (int j = 0; j < ntile; ++j) {
-    const int buf = j & 1;
-    const bool more = j + 1 < ntile;
-    if (more) load_tile(j + 1);
-    if (active) {
+  // Tiles stream through two register sets and two LDS stages: the loads of
+  // tile j+2 are issued before tile j is computed and land in LDS after tile
+  // j+1's computation, so each load has two tiles of compute to arrive in.
+  // Loads and LDS stores are unconditional (a tile index past the end
+  // re-reads the last tile, whose copy is never read), so the compiler's
+  // wait counts never have to cover both register sets at once.
+  bf16x8 ones;
+#pragma unroll
+  for (int x = 0; x < 8; ++x) ones[x] = (__bf16)1.0f;
+  auto compute = [&](int j, int buf) __attribute__((always_inline)) {
       const uint16_t* kl = k_lds[buf];
       const uint16_t* vl = v_lds[buf];
       i32x4 kf[2][4], vf[8];
@@ -321,36 +341,46 @@ __global__ __launch_bounds__(kWaves * 64) void prefill_kernel(PrefillArgs a) {
         const float m_new = fmaxf(m_run[rb], bmax);
         if (__builtin_amdgcn_ballot_w64(m_new > m_run[rb]) != 0) {
           const float alpha = __builtin_amdgcn_exp2f((m_run[rb] - m_new) * cmul);
-          l_part[rb] *= alpha;
+          lsum[rb] *= alpha;
 #pragma unroll
           for (int nn = 0; nn < 8; ++nn) acc[rb][nn] *= alpha;
           m_run[rb] = m_new;
         }
         const float mc = m_run[rb] * cmul;
         bf16x8 p;
-        float psum = 0.f;
 #pragma unroll
-        for (int x = 0; x < 8; ++x) {
-          const __bf16 pe = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(z[x], cmul, -mc));
-          p[x] = pe;
-          psum += (float)pe;
-        }
-        l_part[rb] += psum;
+        for (int x = 0; x < 8; ++x) p[x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(z[x], cmul, -mc));
+        // the softmax denominator sums the rounded probabilities the PV product uses
+        lsum[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, p, lsum[rb], 0, 0, 0);
 #pragma unroll
         for (int nn = 0; nn < 8; ++nn)
           acc[rb][nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[nn]), p, acc[rb][nn],
                                                                 0, 0, 0);
       }
-    }
-    if (more) store_tile(j + 1, buf ^ 1);
+  };
+  i32x4 kA[NCH], vA[NCH], kB[NCH], vB[NCH];
+  load_tile(0, kA, vA);
+  store_tile(0, 0, kA, vA);
+  load_tile(min(1, ntile - 1), kA, vA);
+  __syncthreads();
+  // buf = j mod 2, a constant in each half of the unrolled loop
+  auto iter = [&](int j, int buf, const i32x4 (&kc)[NCH], const i32x4 (&vc)[NCH], i32x4 (&kn)[NCH],
+                  i32x4 (&vn)[NCH]) __attribute__((always_inline)) {
+    load_tile(min(j + 2, ntile - 1), kn, vn);
+    if (active && j < ntile) compute(j, buf);
+    store_tile(j + 1, buf ^ 1, kc, vc);
     __syncthreads();
+  };
+  for (int j = 0; j < ntile; j += 2) {
+    iter(j, 0, kA, vA, kB, vB);
+    iter(j + 1, 1, kB, vB, kA, vA);
   }
 
   // ---- normalise and store: lane (li, lj) holds dims 16 nn + 4 lj + e of column li ----
   if (!active) return;
 #pragma unroll
   for (int rb = 0; rb < R; ++rb) {
-    const float inv = vsc / xor_sum(l_part[rb]);
+    const float inv = vsc / lsum[rb][0];
     const int qrow = q0 + 16 * rb + li;
     if (qrow >= q1) continue;
     const size_t base = ((size_t)(r0 + qrow) * a.hq + h) * kD + 4 * lj;
@@ -403,6 +433,8 @@ extern "C" int chunked_prefill_attention(const void* q, const void* k_blocks, co
       sh->num_blocks > INT32_MAX)
     return fail(DP_EINVAL, "chunked_prefill_attention: need max_blocks_per_seq * 16 >= max_context_len and "
                            "0 < num_blocks <= INT32_MAX");
+  if (sh->max_context_len > kIdCap * kBS)
+    return fail(DP_ENOTSUP, "chunked_prefill_attention: max_context_len above %d", kIdCap * kBS);
   if (sh->total_q < 0 || sh->total_q > INT32_MAX / 2)
     return fail(DP_EINVAL, "chunked_prefill_attention: total_q out of range");
   if (sh->batch == 0 || sh->total_q == 0) return DP_OK;
@@ -418,7 +450,7 @@ extern "C" int chunked_prefill_attention(const void* q, const void* k_blocks, co
   if (!(scale > 0.0f) || !std::isfinite(scale))
     return fail(DP_EINVAL, "chunked_prefill_attention: scale must be finite and > 0");
 
-  const int QT = sh->query_tile ? sh->query_tile : 64;
+  const int QT = sh->query_tile ? sh->query_tile : 32;  // 32: two workgroups per compute unit
   const int group = sh->n_q_heads / sh->n_kv_heads;
   const int nquad = (group + kWaves - 1) / kWaves;
   // an upper bound of sum_s ceil(n_s / QT); surplus workgroups exit at once
