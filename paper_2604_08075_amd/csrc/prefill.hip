@@ -51,11 +51,13 @@ constexpr int kD = 128;
 constexpr int kBS = 16;
 constexpr int kKT = 32;               // KV tokens per LDS tile (two blocks)
 constexpr int kWaves = 4;             // query heads per workgroup
-constexpr int kKRow = kD + 8;         // LDS row of K, in bf16 (16-byte pad: spreads rows over banks)
-constexpr int kVRow = kKT + 8;        // LDS row of V (one head dimension's 32 tokens + pad)
+// LDS tiles are unpadded, their 16-byte chunks XOR-swizzled by row (see ksw/vsw)
+constexpr int kKRow = kD;             // LDS row of K: one token's 128 dims (16 chunks)
+constexpr int kVRow = kKT;            // LDS row of V: one head dimension's 32 tokens (4 chunks)
 constexpr int kKStage = kKT * kKRow;  // bf16 per K stage
 constexpr int kVStage = kD * kVRow;
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kSlack = 8.0f;        // probabilities may reach 2^8 before the reference max moves
 constexpr int kMaxBatch = 4096;
 constexpr int kIdCap = 4096;          // block ids staged in LDS: contexts up to 65,536 tokens
 
@@ -108,6 +110,15 @@ __device__ __forceinline__ i32x4 zero_tokens_from(i32x4 x, int first, int lim) {
   }
   return x;
 }
+
+// Chunk swizzles.  The sixteen K rows one MFMA reads at once (tokens
+// 8q + 4m + e, q, e = 0..3) land on sixteen different 16-byte bank groups,
+// as do the sixteen V rows 16 nn + li, and so does any eight of them that
+// the LDS may serve in one cycle.
+__device__ __forceinline__ int ksw(int row) { return (row & 3) | (((row >> 3) & 3) << 2); }
+__device__ __forceinline__ int vsw(int row) { return (row >> 2) & 3; }
+__device__ __forceinline__ int kpos(int row, int chunk) { return row * kKRow + ((chunk ^ ksw(row)) << 3); }
+__device__ __forceinline__ int vpos(int row, int chunk) { return row * kVRow + ((chunk ^ vsw(row)) << 3); }
 
 __device__ __forceinline__ uint16_t f32_to_bf16_bits(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
 
@@ -249,25 +260,24 @@ __global__ __launch_bounds__(kWaves * 64, R == 2 ? 2 : 1) void prefill_kernel(Pr
     if constexpr (FP8) {
       const int b = tid >> 7, x = tid & 127;
       // K: token 16b + x/8, dims 16 (x%8) .. +16
-      uint16_t* kd = kl + (16 * b + (x >> 3)) * kKRow + 16 * (x & 7);
-      *(i32x4*)kd = fp8x8_to_bf16(kreg[0][0], kreg[0][1]);
-      *(i32x4*)(kd + 8) = fp8x8_to_bf16(kreg[0][2], kreg[0][3]);
+      const int krow = 16 * b + (x >> 3);
+      *(i32x4*)(kl + kpos(krow, 2 * (x & 7))) = fp8x8_to_bf16(kreg[0][0], kreg[0][1]);
+      *(i32x4*)(kl + kpos(krow, 2 * (x & 7) + 1)) = fp8x8_to_bf16(kreg[0][2], kreg[0][3]);
       // V: dim x, tokens 16b .. +16
-      uint16_t* vd = vl + x * kVRow + 16 * b;
       i32x4 v0 = fp8x8_to_bf16(vreg[0][0], vreg[0][1]), v1 = fp8x8_to_bf16(vreg[0][2], vreg[0][3]);
       if (t0 + kKT > T) {  // the sequence ends inside this tile
         v0 = zero_tokens_from(v0, t0 + 16 * b, T);
         v1 = zero_tokens_from(v1, t0 + 16 * b + 8, T);
       }
-      *(i32x4*)vd = v0;
-      *(i32x4*)(vd + 8) = v1;
+      *(i32x4*)(vl + vpos(x, 2 * b)) = v0;
+      *(i32x4*)(vl + vpos(x, 2 * b + 1)) = v1;
     } else {
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         const int c = tid + 256 * i, b = c >> 8, x = c & 255;
-        *(i32x4*)(kl + (16 * b + (x >> 4)) * kKRow + 8 * (x & 15)) = kreg[i];
+        *(i32x4*)(kl + kpos(16 * b + (x >> 4), x & 15)) = kreg[i];
         const int first = 16 * b + 8 * (x & 1);
-        *(i32x4*)(vl + (x >> 1) * kVRow + first) = t0 + kKT > T ? zero_tokens_from(vreg[i], t0 + first, T) : vreg[i];
+        *(i32x4*)(vl + vpos(x >> 1, first >> 3)) = t0 + kKT > T ? zero_tokens_from(vreg[i], t0 + first, T) : vreg[i];
       }
     }
   };
@@ -275,17 +285,21 @@ __global__ __launch_bounds__(kWaves * 64, R == 2 ? 2 : 1) void prefill_kernel(Pr
   // ---- per-lane LDS offsets of the MFMA operands ----
   // K row of MFMA m, row li: token 8 (li / 4) + 4 m + li % 4, so lane (li, lj)'s
   // scores are tokens 8 lj + 4 m + e: its eight P^T operand values.
-  int koff[2];
+  int koff[2][4], voff[8];
 #pragma unroll
-  for (int m = 0; m < 2; ++m) koff[m] = (8 * (li >> 2) + 4 * m + (li & 3)) * kKRow + 8 * lj;
-  const int voff = li * kVRow + 8 * lj;  // + 16 nn rows
+  for (int m = 0; m < 2; ++m)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) koff[m][c] = kpos(8 * (li >> 2) + 4 * m + (li & 3), 4 * c + lj);
+#pragma unroll
+  for (int nn = 0; nn < 8; ++nn) voff[nn] = vpos(16 * nn + li, lj);
 
   f32x4 acc[R][8];
-  float m_run[R];
+  float m_run[R], mlim[R];  // reference max (raw score) and the scaled score that forces a rescale
   f32x4 lsum[R];  // column sums of P, accumulated by the matrix cores (every row holds the sum)
 #pragma unroll
   for (int rb = 0; rb < R; ++rb) {
     m_run[rb] = -INFINITY;
+    mlim[rb] = -INFINITY;
     lsum[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int nn = 0; nn < 8; ++nn) acc[rb][nn] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -307,9 +321,9 @@ __global__ __launch_bounds__(kWaves * 64, R == 2 ? 2 : 1) void prefill_kernel(Pr
 #pragma unroll
       for (int m = 0; m < 2; ++m)
 #pragma unroll
-        for (int c = 0; c < 4; ++c) kf[m][c] = *(const i32x4*)(kl + koff[m] + 32 * c);
+        for (int c = 0; c < 4; ++c) kf[m][c] = *(const i32x4*)(kl + koff[m][c]);
 #pragma unroll
-      for (int nn = 0; nn < 8; ++nn) vf[nn] = *(const i32x4*)(vl + voff + 16 * nn * kVRow);
+      for (int nn = 0; nn < 8; ++nn) vf[nn] = *(const i32x4*)(vl + voff[nn]);
       const int tok0 = kKT * j + 8 * lj;            // token of this lane's score e = 0, m = 0
       const bool diag = kKT * j + kKT - 1 > p_first;  // some (token, query) pair is in the future
 #pragma unroll
@@ -334,17 +348,21 @@ __global__ __launch_bounds__(kWaves * 64, R == 2 ? 2 : 1) void prefill_kernel(Pr
           for (int x = 0; x < 8; ++x)
             if (tok0 + x > pcol) z[x] = -INFINITY;
         }
-        float bmax = z[0];
+        // Lazy rescale: the reference max m_run only moves when some score
+        // exceeds it by more than 2^kSlack in probability (then to the exact
+        // column max), so probabilities stay below 2^kSlack and the common
+        // path needs no cross-lane reduction and no rescale of the accumulators.
+        float lmax = z[0];
 #pragma unroll
-        for (int x = 1; x < 8; ++x) bmax = fmaxf(bmax, z[x]);
-        bmax = xor_max(bmax);
-        const float m_new = fmaxf(m_run[rb], bmax);
-        if (__builtin_amdgcn_ballot_w64(m_new > m_run[rb]) != 0) {
+        for (int x = 1; x < 8; ++x) lmax = fmaxf(lmax, z[x]);
+        if (__builtin_amdgcn_ballot_w64(lmax * cmul > mlim[rb]) != 0) {
+          const float m_new = fmaxf(m_run[rb], xor_max(lmax));
           const float alpha = __builtin_amdgcn_exp2f((m_run[rb] - m_new) * cmul);
           lsum[rb] *= alpha;
 #pragma unroll
           for (int nn = 0; nn < 8; ++nn) acc[rb][nn] *= alpha;
           m_run[rb] = m_new;
+          mlim[rb] = m_new * cmul + kSlack;
         }
         const float mc = m_run[rb] * cmul;
         bf16x8 p;
