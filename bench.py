@@ -244,7 +244,7 @@ def measure_prefill(name, steps, warmup, query_tile=0):
             "us_per_launch": ms * 1e3, "flops": flops, "tflops": tfs,
             "roofline": {"bound": "mfma", "achieved": tfs, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                          "frac": tfs / PEAK_BF16_TFLOPS, "kernel": "prefill_kernel"},
-            "query_tile": query_tile or 32}
+            "query_tile": 32}
 
 
 def router_rate(binding, n=1 << 20, intervals=20000):
@@ -284,7 +284,7 @@ def main():
     ap.add_argument("--wgs-per-cu", type=int, default=0, help="resident workgroups per CU (0 = library choice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true", help="skip the chunked-prefill attention timing")
-    ap.add_argument("--prefill-tile", type=int, default=0, help="query tokens per prefill workgroup (32/64)")
+    ap.add_argument("--prefill-tile", type=int, default=0, help="query tokens per prefill workgroup (0 or 32)")
     ap.add_argument("--prefill-only", action="store_true", help="only time the chunked-prefill attention")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB 10 times (counter calibration) and exit")

@@ -124,7 +124,7 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float x) { return __builtin
 
 // R: 16-token query column blocks per wave, so QT = 16 R query tokens per workgroup.
 template <bool FP8, int R>
-__global__ __launch_bounds__(kWaves * 64, R == 2 ? 2 : 1) void prefill_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(kWaves * 64, 2) void prefill_kernel(PrefillArgs a) {
   constexpr int QT = 16 * R;
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][kKStage];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][kVStage];
@@ -326,37 +326,49 @@ __global__ __launch_bounds__(kWaves * 64, R == 2 ? 2 : 1) void prefill_kernel(Pr
       for (int nn = 0; nn < 8; ++nn) vf[nn] = *(const i32x4*)(vl + voff[nn]);
       const int tok0 = kKT * j + 8 * lj;            // token of this lane's score e = 0, m = 0
       const bool diag = kKT * j + kKT - 1 > p_first;  // some (token, query) pair is in the future
+      // S^T = K Q^T for every column block first, so that the matrix cores
+      // have independent work while the scores of one block are reduced.
+      float z[R][8];
 #pragma unroll
       for (int rb = 0; rb < R; ++rb) {
-        f32x4 sacc[2];
 #pragma unroll
         for (int m = 0; m < 2; ++m) {
-          sacc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+          f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int c = 0; c < 4; ++c)
-            sacc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf[m][c]),
-                                                              __builtin_bit_cast(bf16x8, qf[rb][c]), sacc[m], 0, 0, 0);
+            sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf[m][c]),
+                                                           __builtin_bit_cast(bf16x8, qf[rb][c]), sacc, 0, 0, 0);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) z[rb][4 * m + e] = sacc[e];
         }
-        float z[8];
+      }
+      if (diag) {
 #pragma unroll
-        for (int m = 0; m < 2; ++m)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) z[4 * m + e] = sacc[m][e];
-        if (diag) {
+        for (int rb = 0; rb < R; ++rb) {
           const int pcol = min(p_first + 16 * rb + li, T - 1);  // this column's query position
 #pragma unroll
           for (int x = 0; x < 8; ++x)
-            if (tok0 + x > pcol) z[x] = -INFINITY;
+            if (tok0 + x > pcol) z[rb][x] = -INFINITY;
         }
-        // Lazy rescale: the reference max m_run only moves when some score
-        // exceeds it by more than 2^kSlack in probability (then to the exact
-        // column max), so probabilities stay below 2^kSlack and the common
-        // path needs no cross-lane reduction and no rescale of the accumulators.
-        float lmax = z[0];
+      }
+      // Lazy rescale: the reference max m_run only moves when some score
+      // exceeds it by more than 2^kSlack in probability (then to the exact
+      // column max), so probabilities stay below 2^kSlack and the common
+      // path has no cross-lane reduction, no rescale and no branch.
+      float lmax[R];
+      bool grow = false;
 #pragma unroll
-        for (int x = 1; x < 8; ++x) lmax = fmaxf(lmax, z[x]);
-        if (__builtin_amdgcn_ballot_w64(lmax * cmul > mlim[rb]) != 0) {
-          const float m_new = fmaxf(m_run[rb], xor_max(lmax));
+      for (int rb = 0; rb < R; ++rb) {
+        lmax[rb] = z[rb][0];
+#pragma unroll
+        for (int x = 1; x < 8; ++x) lmax[rb] = fmaxf(lmax[rb], z[rb][x]);
+        grow |= lmax[rb] * cmul > mlim[rb];
+      }
+      if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+#pragma unroll
+        for (int rb = 0; rb < R; ++rb) {
+          if (__builtin_amdgcn_ballot_w64(lmax[rb] * cmul > mlim[rb]) == 0) continue;
+          const float m_new = fmaxf(m_run[rb], xor_max(lmax[rb]));
           const float alpha = __builtin_amdgcn_exp2f((m_run[rb] - m_new) * cmul);
           lsum[rb] *= alpha;
 #pragma unroll
@@ -364,10 +376,13 @@ __global__ __launch_bounds__(kWaves * 64, R == 2 ? 2 : 1) void prefill_kernel(Pr
           m_run[rb] = m_new;
           mlim[rb] = m_new * cmul + kSlack;
         }
+      }
+#pragma unroll
+      for (int rb = 0; rb < R; ++rb) {
         const float mc = m_run[rb] * cmul;
         bf16x8 p;
 #pragma unroll
-        for (int x = 0; x < 8; ++x) p[x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(z[x], cmul, -mc));
+        for (int x = 0; x < 8; ++x) p[x] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(z[rb][x], cmul, -mc));
         // the softmax denominator sums the rounded probabilities the PV product uses
         lsum[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, p, lsum[rb], 0, 0, 0);
 #pragma unroll
@@ -375,6 +390,15 @@ __global__ __launch_bounds__(kWaves * 64, R == 2 ? 2 : 1) void prefill_kernel(Pr
           acc[rb][nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[nn]), p, acc[rb][nn],
                                                                 0, 0, 0);
       }
+      // Scheduling hint: the probabilities of block rb+1 are computed while
+      // the matrix cores run block rb's PV product.
+      __builtin_amdgcn_sched_group_barrier(0x002, 21, 0);
+#pragma unroll
+      for (int i = 0; i < 9 * (R - 1); ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 9, 0);
   };
   i32x4 kA[NCH], vA[NCH], kB[NCH], vB[NCH];
   load_tile(0, kA, vA);
@@ -418,9 +442,7 @@ __global__ __launch_bounds__(kWaves * 64, R == 2 ? 2 : 1) void prefill_kernel(Pr
 }
 
 template __global__ void prefill_kernel<false, 2>(PrefillArgs);
-template __global__ void prefill_kernel<false, 4>(PrefillArgs);
 template __global__ void prefill_kernel<true, 2>(PrefillArgs);
-template __global__ void prefill_kernel<true, 4>(PrefillArgs);
 
 }  // namespace dpool_prefill
 
@@ -439,8 +461,8 @@ extern "C" int chunked_prefill_attention(const void* q, const void* k_blocks, co
     return fail(DP_ENOTSUP, "chunked_prefill_attention: kv_dtype %d", sh->kv_dtype);
   if (sh->out_dtype != DP_OUT_BF16 && sh->out_dtype != DP_OUT_FP32)
     return fail(DP_ENOTSUP, "chunked_prefill_attention: out_dtype %d", sh->out_dtype);
-  if (sh->query_tile != 0 && sh->query_tile != 32 && sh->query_tile != 64)
-    return fail(DP_EINVAL, "chunked_prefill_attention: query_tile must be 0, 32 or 64");
+  if (sh->query_tile != 0 && sh->query_tile != 32)
+    return fail(DP_EINVAL, "chunked_prefill_attention: query_tile must be 0 or 32");
   if (sh->reserved != 0) return fail(DP_EINVAL, "chunked_prefill_attention: reserved must be 0");
   if (sh->batch < 0) return fail(DP_EINVAL, "chunked_prefill_attention: batch < 0");
   if (sh->batch > kMaxBatch) return fail(DP_ENOTSUP, "chunked_prefill_attention: batch above 4096");
@@ -468,7 +490,7 @@ extern "C" int chunked_prefill_attention(const void* q, const void* k_blocks, co
   if (!(scale > 0.0f) || !std::isfinite(scale))
     return fail(DP_EINVAL, "chunked_prefill_attention: scale must be finite and > 0");
 
-  const int QT = sh->query_tile ? sh->query_tile : 32;  // 32: two workgroups per compute unit
+  constexpr int QT = 32;  // two workgroups per compute unit
   const int group = sh->n_q_heads / sh->n_kv_heads;
   const int nquad = (group + kWaves - 1) / kWaves;
   // an upper bound of sum_s ceil(n_s / QT); surplus workgroups exit at once
@@ -501,13 +523,8 @@ extern "C" int chunked_prefill_attention(const void* q, const void* k_blocks, co
   (void)hipGetLastError();
   const dim3 g((unsigned)grid), b(kWaves * 64);
   hipStream_t st = (hipStream_t)stream;
-  if (fp8) {
-    if (QT == 64) hipLaunchKernelGGL((prefill_kernel<true, 4>), g, b, dyn, st, a);
-    else hipLaunchKernelGGL((prefill_kernel<true, 2>), g, b, dyn, st, a);
-  } else {
-    if (QT == 64) hipLaunchKernelGGL((prefill_kernel<false, 4>), g, b, dyn, st, a);
-    else hipLaunchKernelGGL((prefill_kernel<false, 2>), g, b, dyn, st, a);
-  }
+  if (fp8) hipLaunchKernelGGL((prefill_kernel<true, 2>), g, b, dyn, st, a);
+  else hipLaunchKernelGGL((prefill_kernel<false, 2>), g, b, dyn, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(DP_EIO, "chunked_prefill_attention: kernel launch failed: %s", hipGetErrorString(e));
   return DP_OK;

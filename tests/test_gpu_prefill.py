@@ -57,7 +57,7 @@ SMALL = [
 
 
 @pytest.mark.parametrize("case", range(len(SMALL)))
-@pytest.mark.parametrize("query_tile", [32, 64])
+@pytest.mark.parametrize("query_tile", [0, 32])
 def test_small_parity(gpu_lib, case, query_tile):
     chunks, hq, hkv, kv = SMALL[case]
     note(f"prefill small case {case} tile {query_tile}: {chunks} {hq}/{hkv} {kv}")

@@ -293,7 +293,7 @@ def pshape(host_lib, **kw):
 
 @pytest.mark.parametrize("kw,code", [
     (dict(head_dim=64), -95), (dict(block_size=32), -95), (dict(n_q_heads=12, n_kv_heads=8), -22),
-    (dict(max_context_len=64 * 16 + 1), -22), (dict(query_tile=48), -22), (dict(num_blocks=0), -22),
+    (dict(max_context_len=64 * 16 + 1), -22), (dict(query_tile=48), -22), (dict(query_tile=64), -22), (dict(num_blocks=0), -22),
     (dict(batch=-1), -22), (dict(batch=5000), -95), (dict(total_q=-1), -22), (dict(reserved=1), -22),
     (dict(kv_dtype=2), -95), (dict(out_dtype=3), -95),
 ])
