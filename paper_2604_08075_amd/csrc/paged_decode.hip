@@ -209,13 +209,94 @@ __device__ __forceinline__ void store_out8(const DecodeArgs& a, size_t off, f32x
 // round trip on each level (a long segment can be cut into many pieces).
 constexpr int kFanIn = 8;
 
-// Log-sum-exp fold of n records, by one wave, in record order:
+
+// Log-sum-exp fold of records, by one wave, in record order:
 // M = max_p m_p, w_p = l_p 2^(m_p - M), o = sum_p w_p o_p / sum_p w_p,
-// L = sum_p w_p.  The result goes to the output rows of segment (s, g), or
-// to record slot dst.  slot_of(i) names the i-th record's slot; record
-// own_idx (if >= 0) is this wave's own, read from its LDS staging entry
-// `own` (eight [lane] chunks of 4 floats: dims 16 nn + 4 lj .. + 4 of head
-// li at lane li + 16 lj; then each lane's (m, l)) instead of global memory.
+// L = sum_p w_p.  Each lane folds two (head, 8-value chunk) pairs at a time.
+struct Fold {
+  float M[2], L[2];
+  f32x4 o0[2], o1[2];
+};
+
+__device__ __forceinline__ void fold_init(Fold& F) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    F.M[i] = -INFINITY;
+    F.L[i] = 0.f;
+    F.o0[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    F.o1[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+}
+
+// Fold records 0 .. n-1 in order.  rec(u, m, l, x0, x1) fetches record u's
+// values for both pairs; the fetches of kFanIn records are issued before
+// any of them is folded (one memory round trip per kFanIn records).
+template <class Rec>
+__device__ __forceinline__ void fold_records(Fold& F, int n, Rec rec) {
+  for (int r0 = 0; r0 < n; r0 += kFanIn) {
+    float m[kFanIn][2], l[kFanIn][2];
+    f32x4 x0[kFanIn][2], x1[kFanIn][2];
+#pragma unroll
+    for (int u = 0; u < kFanIn; ++u)
+      if (r0 + u < n) rec(r0 + u, m[u], l[u], x0[u], x1[u]);
+#pragma unroll
+    for (int u = 0; u < kFanIn; ++u) {
+      if (r0 + u < n) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const float M2 = fmaxf(F.M[i], m[u][i]);
+          const float c_old = __builtin_amdgcn_exp2f(F.M[i] - M2);
+          const float c_new = l[u][i] * __builtin_amdgcn_exp2f(m[u][i] - M2);
+          F.o0[i] = F.o0[i] * c_old + x0[u][i] * c_new;
+          F.o1[i] = F.o1[i] * c_old + x1[u][i] * c_new;
+          F.L[i] = F.L[i] * c_old + c_new;
+          F.M[i] = M2;
+        }
+      }
+    }
+  }
+}
+
+// The (head, first dim) of this lane's pairs in pass p0 (idle lanes re-read pair 0).
+__device__ __forceinline__ void pair_of(int p0, int lane, int npairs, int (&hd)[2], int (&d0)[2], bool (&ok)[2]) {
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int p = p0 + lane + 64 * i;
+    ok[i] = p < npairs;
+    const int pp = ok[i] ? p : 0;
+    hd[i] = pp >> 4;
+    d0[i] = (pp & 15) * 8;
+  }
+}
+
+// Record u from global slot `slot`, or (own) from this wave's LDS staging
+// entry `own`: eight [lane] chunks of 4 floats (dims 16 nn + 4 lj .. + 4 of
+// head li at lane li + 16 lj), then each lane's (m, l).
+__device__ __forceinline__ void fetch_record(const DecodeArgs& a, size_t slot, const char* own, const int (&hd)[2],
+                                             const int (&d0)[2], float (&m)[2], float (&l)[2], f32x4 (&x0)[2],
+                                             f32x4 (&x1)[2]) {
+  const int G = a.group;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    if (own) {
+      const float* ml = (const float*)(own + 8192 + hd[i] * 8);
+      m[i] = ml[0];
+      l[i] = ml[1];
+      const int nn = d0[i] >> 4, q = (d0[i] & 15) >> 2;
+      x0[i] = *(const f32x4*)(own + nn * 1024 + (hd[i] + 16 * q) * 16);
+      x1[i] = *(const f32x4*)(own + nn * 1024 + (hd[i] + 16 * (q + 1)) * 16);
+    } else {
+      coherent_load2(a.rec_ml + (slot * G + hd[i]) * 2, m[i], l[i]);
+      const float* ro = a.rec_o + (slot * G + hd[i]) * kHeadDim + d0[i];
+      x0[i] = coherent_load4(ro);
+      x1[i] = coherent_load4(ro + 4);
+    }
+  }
+}
+
+// Merge n records (slot_of(i) names the i-th; record own_idx, if >= 0, is
+// this wave's LDS entry `own`) into the output rows of segment (s, g), or
+// into record slot dst.
 template <class SlotOf>
 __device__ __forceinline__ void merge_records(const DecodeArgs& a, SlotOf slot_of, int n, bool to_out, int s, int g,
                                               size_t dst, int lane, int own_idx = -1, const char* own = nullptr) {
@@ -224,68 +305,81 @@ __device__ __forceinline__ void merge_records(const DecodeArgs& a, SlotOf slot_o
   for (int p0 = 0; p0 < npairs; p0 += 128) {  // two pairs per lane at a time
     int hd[2], d0[2];
     bool ok[2];
-    for (int i = 0; i < 2; ++i) {
-      const int p = p0 + lane + 64 * i;
-      ok[i] = p < npairs;
-      const int pp = ok[i] ? p : 0;  // idle lanes re-read pair 0 and discard it
-      hd[i] = pp >> 4;
-      d0[i] = (pp & 15) * 8;
-    }
-    float M[2] = {-INFINITY, -INFINITY}, L[2] = {0.f, 0.f};
-    f32x4 o0[2] = {}, o1[2] = {};
-    for (int r0 = 0; r0 < n; r0 += kFanIn) {
-      float m[kFanIn][2], l[kFanIn][2];
-      f32x4 x0[kFanIn][2], x1[kFanIn][2];
-#pragma unroll
-      for (int u = 0; u < kFanIn; ++u) {
-        if (r0 + u == own_idx) {
-#pragma unroll
-          for (int i = 0; i < 2; ++i) {
-            const float* ml = (const float*)(own + 8192 + hd[i] * 8);
-            m[u][i] = ml[0];
-            l[u][i] = ml[1];
-            const int nn = d0[i] >> 4, q = (d0[i] & 15) >> 2;
-            x0[u][i] = *(const f32x4*)(own + nn * 1024 + (hd[i] + 16 * q) * 16);
-            x1[u][i] = *(const f32x4*)(own + nn * 1024 + (hd[i] + 16 * (q + 1)) * 16);
-          }
-        } else if (r0 + u < n) {
-          const size_t slot = slot_of(r0 + u);
-#pragma unroll
-          for (int i = 0; i < 2; ++i) {
-            coherent_load2(a.rec_ml + (slot * G + hd[i]) * 2, m[u][i], l[u][i]);
-            const float* ro = a.rec_o + (slot * G + hd[i]) * kHeadDim + d0[i];
-            x0[u][i] = coherent_load4(ro);
-            x1[u][i] = coherent_load4(ro + 4);
-          }
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < kFanIn; ++u) {
-        if (r0 + u < n) {
-#pragma unroll
-          for (int i = 0; i < 2; ++i) {
-            const float M2 = fmaxf(M[i], m[u][i]);
-            const float c_old = __builtin_amdgcn_exp2f(M[i] - M2);
-            const float c_new = l[u][i] * __builtin_amdgcn_exp2f(m[u][i] - M2);
-            o0[i] = o0[i] * c_old + x0[u][i] * c_new;
-            o1[i] = o1[i] * c_old + x1[u][i] * c_new;
-            L[i] = L[i] * c_old + c_new;
-            M[i] = M2;
-          }
-        }
-      }
-    }
+    pair_of(p0, lane, npairs, hd, d0, ok);
+    Fold F;
+    fold_init(F);
+    fold_records(F, n, [&](int u, float(&m)[2], float(&l)[2], f32x4(&x0)[2], f32x4(&x1)[2])
+                           __attribute__((always_inline)) {
+                             fetch_record(a, u == own_idx ? 0 : slot_of(u), u == own_idx ? own : nullptr, hd, d0, m, l,
+                                          x0, x1);
+                           });
     for (int i = 0; i < 2; ++i) {
       if (!ok[i]) continue;
-      const float inv = 1.0f / L[i];
+      const float inv = 1.0f / F.L[i];
       if (to_out) {
-        store_out8(a, ((size_t)s * a.hq + (size_t)g * G + hd[i]) * kHeadDim + d0[i], o0[i] * inv, o1[i] * inv);
+        store_out8(a, ((size_t)s * a.hq + (size_t)g * G + hd[i]) * kHeadDim + d0[i], F.o0[i] * inv, F.o1[i] * inv);
       } else {
         float* ro = a.rec_o + (dst * G + hd[i]) * kHeadDim + d0[i];
-        coherent_store4(ro, o0[i] * inv);
-        coherent_store4(ro + 4, o1[i] * inv);
-        if (d0[i] == 0) coherent_store2(a.rec_ml + (dst * G + hd[i]) * 2, M[i], L[i]);
+        coherent_store4(ro, F.o0[i] * inv);
+        coherent_store4(ro + 4, F.o1[i] * inv);
+        if (d0[i] == 0) coherent_store2(a.rec_ml + (dst * G + hd[i]) * 2, F.M[i], F.L[i]);
       }
+    }
+  }
+}
+
+// Both merge levels at once, by the wave that completes the last group of a
+// segment: its group's members are folded (record own_idx from LDS) into the
+// values the group record would hold, and those take group c_own's place in
+// the fold of all groups into the output rows.  The result is bit-identical
+// to storing the group record and merging it from memory.
+template <class MemberOf, class GroupOf>
+__device__ __forceinline__ void merge_group_then_segment(const DecodeArgs& a, MemberOf member_of, int gn, int own_idx,
+                                                         const char* own, GroupOf group_of, int ngroups, int c_own,
+                                                         int s, int g, int lane) {
+  const int G = a.group;
+  const int npairs = G * 16;
+  for (int p0 = 0; p0 < npairs; p0 += 128) {
+    int hd[2], d0[2];
+    bool ok[2];
+    pair_of(p0, lane, npairs, hd, d0, ok);
+    Fold Fg;
+    fold_init(Fg);
+    fold_records(Fg, gn, [&](int u, float(&m)[2], float(&l)[2], f32x4(&x0)[2], f32x4(&x1)[2])
+                             __attribute__((always_inline)) {
+                               fetch_record(a, u == own_idx ? 0 : member_of(u), u == own_idx ? own : nullptr, hd, d0, m,
+                                            l, x0, x1);
+                             });
+    float gm[2], gl[2];
+    f32x4 gx0[2], gx1[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {  // exactly what the group record would hold
+      const float inv = 1.0f / Fg.L[i];
+      gx0[i] = Fg.o0[i] * inv;
+      gx1[i] = Fg.o1[i] * inv;
+      gm[i] = Fg.M[i];
+      gl[i] = Fg.L[i];
+    }
+    Fold F;
+    fold_init(F);
+    fold_records(F, ngroups, [&](int u, float(&m)[2], float(&l)[2], f32x4(&x0)[2], f32x4(&x1)[2])
+                                 __attribute__((always_inline)) {
+                                   if (u == c_own) {
+#pragma unroll
+                                     for (int i = 0; i < 2; ++i) {
+                                       m[i] = gm[i];
+                                       l[i] = gl[i];
+                                       x0[i] = gx0[i];
+                                       x1[i] = gx1[i];
+                                     }
+                                   } else {
+                                     fetch_record(a, group_of(u), nullptr, hd, d0, m, l, x0, x1);
+                                   }
+                                 });
+    for (int i = 0; i < 2; ++i) {
+      if (!ok[i]) continue;
+      const float inv = 1.0f / F.L[i];
+      store_out8(a, ((size_t)s * a.hq + (size_t)g * G + hd[i]) * kHeadDim + d0[i], F.o0[i] * inv, F.o1[i] * inv);
     }
   }
 }
@@ -737,8 +831,10 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   // Pieces are merged in groups of kFanIn consecutive pieces, then the groups.
   // Piece r of a segment is wave k0 + r's; a group's counter and record slot
   // belong to the wave of its last piece (whose piece is that wave's first).
-  int* const group_cnt = a.arrivals;
-  int* const seg_cnt = a.arrivals + TW;
+  int* const group_base = a.arrivals;
+  int* const seg_base = a.arrivals + TW;
+  auto group_cnt = [&](int k) __attribute__((always_inline)) { return group_base + k; };
+  auto seg_cnt = [&](int k) __attribute__((always_inline)) { return seg_base + k; };
   struct SegInfo {
     int k0, kend, np, first_slot, r, gfirst, gn, kg, ngroups;
   };
@@ -766,7 +862,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   if (own_entry >= 0) {
     own_f = seg_info(own_x == 0 ? arr_s0 : arr_s1, own_x == 0 ? arr_g0 : arr_g1);
     int c = 0;
-    if (lane == 0) c = __hip_atomic_load(group_cnt + own_f.kg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (lane == 0) c = __hip_atomic_load(group_cnt(own_f.kg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     own_last = __shfl(c, 0) == own_f.gn - 1;
   }
   flush(own_last ? own_entry : -1);
@@ -775,37 +871,63 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     // before it counts them
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     const char* own_rec = own_entry >= 0 ? stg + (__builtin_amdgcn_readfirstlane(stage_kind[w][own_entry]) >> 4) : nullptr;
+    // Both pieces' arrivals are counted before either count is examined:
+    // a device-wide atomic takes a few microseconds to return, and the two
+    // would otherwise follow one another.
+    SegInfo f0 = {}, f1 = {};
+    int old0 = 0, old1 = 0;
+    if (arr_s0 >= 0) {
+      const bool mine = own_last && own_x == 0;
+      f0 = mine ? own_f : seg_info(arr_s0, arr_g0);
+      if (!mine && lane == 0)
+        old0 = __hip_atomic_fetch_add(group_cnt(f0.kg), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (arr_s1 >= 0) {
+      const bool mine = own_last && own_x == 1;
+      f1 = mine ? own_f : seg_info(arr_s1, arr_g1);
+      if (!mine && lane == 0)
+        old1 = __hip_atomic_fetch_add(group_cnt(f1.kg), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     for (int x = 0; x < 2; ++x) {
       const int s = x == 0 ? arr_s0 : arr_s1;
       if (s < 0) continue;
       const int g = x == 0 ? arr_g0 : arr_g1;
       const bool mine = own_last && x == own_x;
-      const SegInfo f = mine ? own_f : seg_info(s, g);
+      const SegInfo f = x == 0 ? f0 : f1;
       auto piece_slot = [&](int r) __attribute__((always_inline)) {
         return r == 0 ? (size_t)f.first_slot : (size_t)2 * (f.k0 + r);
       };
-      if (!mine) {
-        int old = 0;
-        if (lane == 0) old = __hip_atomic_fetch_add(group_cnt + f.kg, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (__shfl(old, 0) != f.gn - 1) continue;  // not the group's last arrival
-      }
+      if (!mine && __shfl(x == 0 ? old0 : old1, 0) != f.gn - 1) continue;  // not the group's last arrival
       asm volatile("" ::: "memory");  // record loads are issued after this branch resolves
-      if (lane == 0) __hip_atomic_store(group_cnt + f.kg, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (lane == 0) __hip_atomic_store(group_cnt(f.kg), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (f.ngroups == 1) {
         merge_records(a, piece_slot, f.np, true, s, g, 0, lane, mine ? f.r : -1, own_rec);
         continue;
       }
-      merge_records(a, [&](int i) __attribute__((always_inline)) { return piece_slot(f.gfirst + i); }, f.gn, false, s,
-                    g, (size_t)2 * TW + f.kg, lane, mine ? f.r - f.gfirst : -1, own_rec);
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      int old = 0;
-      if (lane == 0) old = __hip_atomic_fetch_add(seg_cnt + f.kend, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (__shfl(old, 0) != f.ngroups - 1) continue;
-      asm volatile("" ::: "memory");
-      if (lane == 0) __hip_atomic_store(seg_cnt + f.kend, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      auto member_slot = [&](int i) __attribute__((always_inline)) { return piece_slot(f.gfirst + i); };
       auto group_slot = [&](int c) __attribute__((always_inline)) {
         return (size_t)2 * TW + f.k0 + min(f.np, (c + 1) * kFanIn) - 1;
       };
+      // If every other group of the segment is already merged, merge this
+      // group and the segment in one pass: no group record, no wait for its
+      // store, no second counter round trip.
+      int done = 0;
+      if (lane == 0) done = __hip_atomic_load(seg_cnt(f.kend), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (__shfl(done, 0) == f.ngroups - 1) {
+        asm volatile("" ::: "memory");  // group record loads are issued after this branch resolves
+        if (lane == 0) __hip_atomic_store(seg_cnt(f.kend), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        merge_group_then_segment(a, member_slot, f.gn, mine ? f.r - f.gfirst : -1, own_rec, group_slot, f.ngroups,
+                                 f.gfirst / kFanIn, s, g, lane);
+        continue;
+      }
+      merge_records(a, member_slot, f.gn, false, s, g, (size_t)2 * TW + f.kg, lane, mine ? f.r - f.gfirst : -1,
+                    own_rec);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      int old = 0;
+      if (lane == 0) old = __hip_atomic_fetch_add(seg_cnt(f.kend), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (__shfl(old, 0) != f.ngroups - 1) continue;
+      asm volatile("" ::: "memory");
+      if (lane == 0) __hip_atomic_store(seg_cnt(f.kend), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       merge_records(a, group_slot, f.ngroups, true, s, g, 0, lane);
     }
   }
