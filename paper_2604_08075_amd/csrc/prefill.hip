@@ -231,24 +231,29 @@ __global__ __launch_bounds__(kWaves * 64, 2) void prefill_kernel(PrefillArgs a) 
     ids_lds[i] = id < 0 ? 0 : (id > a.num_blocks_m1 ? a.num_blocks_m1 : id);
   }
   __syncthreads();
-  auto block_id = [&](int j, int b) __attribute__((always_inline)) {
+  // The tile's block ids are the same for a whole wave: read once, kept in
+  // scalar registers, so the loads address a uniform base plus a fixed lane
+  // offset.
+  auto tile_base = [&](int j, int b) __attribute__((always_inline)) {
     int bi = 2 * j + b;
     if (bi >= nb) bi = 2 * j;  // a block past the sequence re-reads the tile's first (then zeroed / masked)
-    return (size_t)ids_lds[bi] * a.hkv + g;
+    return __builtin_amdgcn_readfirstlane(ids_lds[bi]) * a.hkv + g;
   };
+  // per-lane byte offsets inside a (block, head) tile, fixed for the kernel
+  const int kx = FP8 ? ((tid & 127) >> 3) * 128 + (tid & 7) * 16 : (tid >> 4) * 256 + (tid & 15) * 16;
+  const int vx = FP8 ? (tid & 127) * 16 : (tid >> 1) * 32 + (tid & 1) * 16;
   auto load_tile = [&](int j, i32x4 (&kreg)[NCH], i32x4 (&vreg)[NCH]) __attribute__((always_inline)) {
     if constexpr (FP8) {
-      const int b = tid >> 7, x = tid & 127;
-      const size_t tile = block_id(j, b);
-      kreg[0] = *(const i32x4*)(a.k + tile * 2048 + (x >> 3) * 128 + (x & 7) * 16);
-      vreg[0] = *(const i32x4*)(a.v + tile * 2048 + x * 16);
+      // waves 0, 1 copy the tile's first block, waves 2, 3 its second
+      const size_t tile = (size_t)tile_base(j, w >> 1);
+      kreg[0] = *(const i32x4*)(a.k + tile * 2048 + kx);
+      vreg[0] = *(const i32x4*)(a.v + tile * 2048 + vx);
     } else {
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int c = tid + 256 * i, b = c >> 8, x = c & 255;
-        const size_t tile = block_id(j, b);
-        kreg[i] = *(const i32x4*)(a.k + tile * 4096 + (x >> 4) * 256 + (x & 15) * 16);
-        vreg[i] = *(const i32x4*)(a.v + tile * 4096 + (x >> 1) * 32 + (x & 1) * 16);
+      for (int i = 0; i < 2; ++i) {  // chunk i of every thread lies in block i of the tile
+        const size_t tile = (size_t)tile_base(j, i);
+        kreg[i] = *(const i32x4*)(a.k + tile * 4096 + kx);
+        vreg[i] = *(const i32x4*)(a.v + tile * 4096 + vx);
       }
     }
   };
