@@ -12,10 +12,10 @@
 //
 // Unlike decode, a chunk reuses every K/V tile for many query rows, so the
 // work is a dense contraction and belongs on the matrix cores.  One
-// workgroup of four waves takes one tile of QT query tokens of one sequence
-// and four query heads of one GQA group (one head per wave: the K/V tile
-// staged in LDS feeds 4 * QT (query, head) columns).  Per 32-token KV tile:
-//   * all 256 threads copy the two 16-token blocks of K and V from the cache
+// workgroup of eight waves takes one tile of QT query tokens of one sequence
+// and eight query heads of one GQA group (one head per wave: the K/V tile
+// staged in LDS feeds 8 * QT (query, head) columns).  Per 32-token KV tile:
+//   * all 512 threads copy the two 16-token blocks of K and V from the cache
 //     into LDS (fp8 widened to bf16 on the way, exactly), double buffered:
 //     the next tile's global loads are in flight while the current one is
 //     computed, and one barrier per tile separates the two;
@@ -50,7 +50,7 @@ typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
 constexpr int kD = 128;
 constexpr int kBS = 16;
 constexpr int kKT = 32;               // KV tokens per LDS tile (two blocks)
-constexpr int kWaves = 4;             // query heads per workgroup
+constexpr int kWaves = 8;             // query heads per workgroup
 // LDS tiles are unpadded, their 16-byte chunks XOR-swizzled by row (see ksw/vsw)
 constexpr int kKRow = kD;             // LDS row of K: one token's 128 dims (16 chunks)
 constexpr int kVRow = kKT;            // LDS row of V: one head dimension's 32 tokens (4 chunks)
@@ -124,7 +124,7 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float x) { return __builtin
 
 // R: 16-token query column blocks per wave, so QT = 16 R query tokens per workgroup.
 template <bool FP8, int R>
-__global__ __launch_bounds__(kWaves * 64, 2) void prefill_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(kWaves * 64, 1) void prefill_kernel(PrefillArgs a) {
   constexpr int QT = 16 * R;
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][kKStage];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][kVStage];
@@ -221,7 +221,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void prefill_kernel(PrefillArgs a) 
   }
 
   // ---- cooperative tile copy: cache -> registers -> LDS ----
-  constexpr int NCH = FP8 ? 1 : 2;  // 16-byte chunks per thread, each of K and V
+  constexpr int NCH = 1;  // 16-byte chunks per thread, each of K and V (fp8: waves 0-3 copy K, 4-7 V)
   // Block ids come from LDS, staged once: a block-table load inside the loop
   // would sit behind the tile loads on the in-order memory counter, and
   // waiting for it would drain the tile prefetch.
@@ -240,21 +240,18 @@ __global__ __launch_bounds__(kWaves * 64, 2) void prefill_kernel(PrefillArgs a) 
     return __builtin_amdgcn_readfirstlane(ids_lds[bi]) * a.hkv + g;
   };
   // per-lane byte offsets inside a (block, head) tile, fixed for the kernel
-  const int kx = FP8 ? ((tid & 127) >> 3) * 128 + (tid & 7) * 16 : (tid >> 4) * 256 + (tid & 15) * 16;
-  const int vx = FP8 ? (tid & 127) * 16 : (tid >> 1) * 32 + (tid & 1) * 16;
+  const int kx = FP8 ? ((tid & 127) >> 3) * 128 + (tid & 7) * 16 : ((tid & 255) >> 4) * 256 + (tid & 15) * 16;
+  const int vx = FP8 ? (tid & 127) * 16 : ((tid & 255) >> 1) * 32 + (tid & 1) * 16;
   auto load_tile = [&](int j, i32x4 (&kreg)[NCH], i32x4 (&vreg)[NCH]) __attribute__((always_inline)) {
     if constexpr (FP8) {
-      // waves 0, 1 copy the tile's first block, waves 2, 3 its second
-      const size_t tile = (size_t)tile_base(j, w >> 1);
-      kreg[0] = *(const i32x4*)(a.k + tile * 2048 + kx);
-      vreg[0] = *(const i32x4*)(a.v + tile * 2048 + vx);
+      // waves 0-3 copy K, 4-7 V; waves 4m, 4m+1 the tile's first block, 4m+2, 4m+3 its second
+      const size_t tile = (size_t)tile_base(j, (w >> 1) & 1);
+      if (w < 4) kreg[0] = *(const i32x4*)(a.k + tile * 2048 + kx);
+      else vreg[0] = *(const i32x4*)(a.v + tile * 2048 + vx);
     } else {
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {  // chunk i of every thread lies in block i of the tile
-        const size_t tile = (size_t)tile_base(j, i);
-        kreg[i] = *(const i32x4*)(a.k + tile * 4096 + kx);
-        vreg[i] = *(const i32x4*)(a.v + tile * 4096 + vx);
-      }
+      const size_t tile = (size_t)tile_base(j, w >> 2);  // waves 0-3: first block, 4-7: second
+      kreg[0] = *(const i32x4*)(a.k + tile * 4096 + kx);
+      vreg[0] = *(const i32x4*)(a.v + tile * 4096 + vx);
     }
   };
   auto store_tile = [&](int j, int buf, const i32x4 (&kreg)[NCH], const i32x4 (&vreg)[NCH])
@@ -263,27 +260,27 @@ __global__ __launch_bounds__(kWaves * 64, 2) void prefill_kernel(PrefillArgs a) 
     uint16_t* vl = v_lds[buf];
     const int t0 = kKT * j;
     if constexpr (FP8) {
-      const int b = tid >> 7, x = tid & 127;
-      // K: token 16b + x/8, dims 16 (x%8) .. +16
-      const int krow = 16 * b + (x >> 3);
-      *(i32x4*)(kl + kpos(krow, 2 * (x & 7))) = fp8x8_to_bf16(kreg[0][0], kreg[0][1]);
-      *(i32x4*)(kl + kpos(krow, 2 * (x & 7) + 1)) = fp8x8_to_bf16(kreg[0][2], kreg[0][3]);
-      // V: dim x, tokens 16b .. +16
-      i32x4 v0 = fp8x8_to_bf16(vreg[0][0], vreg[0][1]), v1 = fp8x8_to_bf16(vreg[0][2], vreg[0][3]);
-      if (t0 + kKT > T) {  // the sequence ends inside this tile
-        v0 = zero_tokens_from(v0, t0 + 16 * b, T);
-        v1 = zero_tokens_from(v1, t0 + 16 * b + 8, T);
+      const int b = (w >> 1) & 1, x = tid & 127;
+      if (w < 4) {
+        // K: token 16b + x/8, dims 16 (x%8) .. +16
+        const int krow = 16 * b + (x >> 3);
+        *(i32x4*)(kl + kpos(krow, 2 * (x & 7))) = fp8x8_to_bf16(kreg[0][0], kreg[0][1]);
+        *(i32x4*)(kl + kpos(krow, 2 * (x & 7) + 1)) = fp8x8_to_bf16(kreg[0][2], kreg[0][3]);
+      } else {
+        // V: dim x, tokens 16b .. +16
+        i32x4 v0 = fp8x8_to_bf16(vreg[0][0], vreg[0][1]), v1 = fp8x8_to_bf16(vreg[0][2], vreg[0][3]);
+        if (t0 + kKT > T) {  // the sequence ends inside this tile
+          v0 = zero_tokens_from(v0, t0 + 16 * b, T);
+          v1 = zero_tokens_from(v1, t0 + 16 * b + 8, T);
+        }
+        *(i32x4*)(vl + vpos(x, 2 * b)) = v0;
+        *(i32x4*)(vl + vpos(x, 2 * b + 1)) = v1;
       }
-      *(i32x4*)(vl + vpos(x, 2 * b)) = v0;
-      *(i32x4*)(vl + vpos(x, 2 * b + 1)) = v1;
     } else {
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int c = tid + 256 * i, b = c >> 8, x = c & 255;
-        *(i32x4*)(kl + kpos(16 * b + (x >> 4), x & 15)) = kreg[i];
-        const int first = 16 * b + 8 * (x & 1);
-        *(i32x4*)(vl + vpos(x >> 1, first >> 3)) = t0 + kKT > T ? zero_tokens_from(vreg[i], t0 + first, T) : vreg[i];
-      }
+      const int b = w >> 2, x = tid & 255;
+      *(i32x4*)(kl + kpos(16 * b + (x >> 4), x & 15)) = kreg[0];
+      const int first = 16 * b + 8 * (x & 1);
+      *(i32x4*)(vl + vpos(x >> 1, first >> 3)) = t0 + kKT > T ? zero_tokens_from(vreg[0], t0 + first, T) : vreg[0];
     }
   };
 
@@ -495,7 +492,7 @@ extern "C" int chunked_prefill_attention(const void* q, const void* k_blocks, co
   if (!(scale > 0.0f) || !std::isfinite(scale))
     return fail(DP_EINVAL, "chunked_prefill_attention: scale must be finite and > 0");
 
-  constexpr int QT = 32;  // two workgroups per compute unit
+  constexpr int QT = 32;  // one eight-wave workgroup per compute unit, two waves per SIMD
   const int group = sh->n_q_heads / sh->n_kv_heads;
   const int nquad = (group + kWaves - 1) / kWaves;
   // an upper bound of sum_s ceil(n_s / QT); surplus workgroups exit at once
