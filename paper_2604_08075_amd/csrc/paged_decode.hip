@@ -1037,9 +1037,12 @@ int validate(const dp_decode_shape* sh, Plan* plan) {
   if (max_units > INT32_MAX) return fail(DP_ENOTSUP, "paged_decode: %lld units exceed int32", (long long)max_units);
   plan->unit_tokens = unit;
   plan->min_chunk = P ? P / unit : 1;
-  // LDS per workgroup: tile lists + wave sums (static) + unit prefix,
-  // context lengths and fp8 scales (dynamic)
-  const size_t stat = (size_t)kWaves * kMaxUnitsPerWave * (fp8 ? 4 : 2) * 4 + 64;
+  // LDS per workgroup: the kernel's static arrays (tile lists, wave sums,
+  // staging of finished rows and records, with 256 bytes for alignment) +
+  // unit prefix, context lengths and fp8 scales (dynamic)
+  const size_t stat = (size_t)kWaves * kMaxUnitsPerWave * (fp8 ? 4 : 2) * sizeof(int) + kWaves * sizeof(int) +
+                      (size_t)kWaves * kStageBytes + (size_t)kWaves * kMaxStaged * (sizeof(long long) + sizeof(int)) +
+                      256;
   plan->dyn_lds = (size_t)(2 * sh->batch + 1 + 2 * sh->n_kv_heads) * 4;
   if (stat + plan->dyn_lds > kLdsBytes)
     return fail(DP_ENOTSUP, "paged_decode: %zu bytes of LDS per workgroup", stat + plan->dyn_lds);
