@@ -235,3 +235,21 @@ def test_workspace_reused_across_shapes(gpu_lib):
     counters = shared[:8 * waves[0]].view(torch.int32)
     assert int(counters.count_nonzero()) == 0
     assert max_err(ref_b, oracle_out(wb), [0, 1, 2]) <= TOL["fp8_e4m3"]
+
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3"])
+def test_largest_batch(gpu_lib, kv):
+    """4,096 sequences (the most one call takes): short and empty contexts, every
+    slice crossing many segments; sampled rows against the oracle, empty rows zero."""
+    note(f"batch 4096, {kv}")
+    rng = np.random.default_rng(31)
+    ctx = rng.integers(0, 97, 4096)
+    ctx[rng.integers(0, 4096, 64)] = 0
+    w = workloads.make_workload(4096, 16, 2, ctx, c_max=128, kv_format=kv, seed=14)
+    got = gpu_out(gpu_lib, w)
+    seqs = sample_seqs(w, 48)
+    err = max_err(got, oracle_out(w, seqs), seqs)
+    note(f"  max abs err {err:.3e}")
+    assert err <= TOL[kv]
+    empty = np.nonzero(w.context_lens == 0)[0]
+    assert len(empty) > 0 and np.all(got[empty] == 0.0)

@@ -123,3 +123,17 @@ def test_deterministic(gpu_lib):
     a = gpu_rows(gpu_lib, w, dev)
     b = gpu_rows(gpu_lib, w, dev)
     np.testing.assert_array_equal(a, b)
+
+
+def test_longest_context(gpu_lib):
+    """A chunk at the end of a 65,536-token context (the longest the kernel stages
+    block ids for), with a ragged last query tile; sampled rows against the oracle."""
+    note("prefill at context 65536")
+    w = workloads.make_prefill([(77, 65536), (40, 1000)], 16, 2, c_max=65536, seed=23)
+    qs = w.meta["q_start"]
+    rows = sorted({0, 1, 31, 32, 63, 64, 76, int(qs[1]), int(qs[2]) - 1})
+    got = gpu_rows(gpu_lib, w)
+    ref = oracle_rows(w, rows)
+    err = float(np.abs(got[rows] - ref[rows]).max())
+    note(f"  max abs err {err:.3e}")
+    assert np.isfinite(got).all() and err <= TOL["bf16"]
