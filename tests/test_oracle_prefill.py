@@ -11,6 +11,7 @@ import numpy as np
 import pytest
 import torch
 
+import workloads
 from oracle import attention, numerics, prefill
 from test_oracle_attention import SCALE, codes_bf16, dense_case, dense_gather
 
@@ -23,7 +24,7 @@ def prefill_case(rng, Hq, Hkv, ctx, qlen, kv="bf16"):
     return qb, kb, vb, bt, ctx, q_start
 
 
-def sdpa_causal(qb, kb, vb, bt, ctx, q_start, scale):
+def sdpa_causal(qb, kb, vb, bt, ctx, q_start, scale, fmt="bf16", ks=None, vs=None):
     Hq = qb.shape[1]
     Hkv = kb.shape[1]
     G = Hq // Hkv
@@ -33,8 +34,10 @@ def sdpa_causal(qb, kb, vb, bt, ctx, q_start, scale):
         n, T = r1 - r0, int(ctx[s])
         if n == 0:
             continue
-        K = np.stack([dense_gather(kb, bt, s, g, T) for g in range(Hkv)])
-        V = np.stack([dense_gather(vb, bt, s, g, T, dims_major=True) for g in range(Hkv)])
+        kmul = [1.0] * Hkv if ks is None else [float(x) for x in ks]
+        vmul = [1.0] * Hkv if vs is None else [float(x) for x in vs]
+        K = np.stack([kmul[g] * dense_gather(kb, bt, s, g, T, fmt) for g in range(Hkv)])
+        V = np.stack([vmul[g] * dense_gather(vb, bt, s, g, T, fmt, dims_major=True) for g in range(Hkv)])
         Kt = torch.from_numpy(K).repeat_interleave(G, dim=0)[None]          # [1, Hq, T, D]
         Vt = torch.from_numpy(V).repeat_interleave(G, dim=0)[None]
         Qt = torch.from_numpy(numerics.decode_bf16(qb[r0:r1])).permute(1, 0, 2)[None]   # [1, Hq, n, D]
@@ -88,6 +91,18 @@ def test_library_sdpa_causal(Hq, Hkv, ctx, qlen):
     rng = np.random.default_rng(2)
     case = prefill_case(rng, Hq, Hkv, ctx, qlen)
     np.testing.assert_allclose(run(*case), sdpa_causal(*case, SCALE), rtol=1e-10, atol=1e-12)
+
+
+def test_library_sdpa_causal_gqa16_fp8():
+    """An e4m3 cache with per-head K and V scales (Sec. 4.7's FP8 serving): the
+    oracle against torch SDPA on the decoded, scaled tensors."""
+    w = workloads.make_prefill([(40, 100), (17, 17), (5, 70)], 16, 1, c_max=128, kv_format="fp8_e4m3", seed=17)
+    kb, vb = w.k_store.dense(), w.v_store.dense()
+    got = prefill.chunked_prefill_attention(w.q_bits, kb, vb, w.block_tables, w.context_lens, w.meta["q_start"],
+                                            SCALE, kv_format="fp8_e4m3", k_scale=w.k_scale, v_scale=w.v_scale)
+    ref = sdpa_causal(w.q_bits, kb, vb, w.block_tables, w.context_lens, w.meta["q_start"], SCALE, fmt="fp8_e4m3",
+                      ks=w.k_scale, vs=w.v_scale)
+    np.testing.assert_allclose(got, ref, rtol=1e-10, atol=1e-12)
 
 
 def test_one_token_chunks_are_decode():
