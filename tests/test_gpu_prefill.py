@@ -137,3 +137,21 @@ def test_longest_context(gpu_lib):
     err = float(np.abs(got[rows] - ref[rows]).max())
     note(f"  max abs err {err:.3e}")
     assert np.isfinite(got).all() and err <= TOL["bf16"]
+
+
+@pytest.mark.parametrize("chunks,hq,hkv", [
+    ([(2048, 2048), (2200, 4096)], 8, 2),     # 266 items: a partial second (backward) round
+    ([(3000, 3000), (1500, 2000)], 8, 4),     # 564 items: a partial third (forward) round
+])
+def test_item_rounds_with_a_partial_last_round(gpu_lib, chunks, hq, hkv):
+    """More (query tile, head group) items than workgroups, not a multiple of them:
+    every row is written (the output starts as NaN) and sampled rows match the oracle."""
+    note(f"prefill rounds {chunks} {hq}/{hkv}")
+    w = workloads.make_prefill(chunks, hq, hkv, c_max=4096, seed=29)
+    total_q = int(w.meta["q_start"][-1])
+    rows = sorted(set(range(0, total_q, 97)) | {total_q - 1, int(w.meta["q_start"][1]) - 1, int(w.meta["q_start"][1])})
+    got = gpu_rows(gpu_lib, w)
+    ref = oracle_rows(w, rows)
+    err = float(np.abs(got[rows] - ref[rows]).max())
+    note(f"  max abs err {err:.3e}")
+    assert np.isfinite(got).all() and err <= TOL["bf16"]
