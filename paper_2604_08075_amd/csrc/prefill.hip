@@ -143,10 +143,10 @@ __global__ __launch_bounds__(kWaves * 64, 1) void prefill_kernel(PrefillArgs a) 
   int* const row1 = row0 + B;          // one past its last
   int* const ctx = row1 + B;           // cached tokens (clamped)
 
-  // ---- which (sequence, query tile, KV head, head quad) this workgroup takes ----
+  // ---- the items: (sequence, query tile, KV head, head quad) ----
   // Query tiles are numbered from the end of the batch backwards (the last
   // tile of the last sequence first): later tiles attend more tokens, so
-  // the longest work is dispatched first.
+  // the longest items are handed out first.
   if (tid == 0) tile_pre[0] = 0;
   {
     // exclusive prefix of ceil(n_s / QT) over sequences (serial per 256 sequences: B is small)
