@@ -319,3 +319,32 @@ def test_prefill_bad_pointers_and_scale_rejected_on_host(host_lib):
     empty = pshape(host_lib, total_q=0)
     assert L.chunked_prefill_attention(None, None, None, None, None, None, 1.0, None, None, None,
                                        ctypes.byref(empty), None) == 0   # nothing to do, nothing enqueued
+
+
+# ---------------------------------------------------------------- KV append validation (host only)
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(head_dim=64), -95), (dict(block_size=32), -95), (dict(batch=-1), -22), (dict(num_blocks=0), -22),
+    (dict(n_q_heads=0, n_kv_heads=0), -22), (dict(max_blocks_per_seq=0, max_context_len=0), -22),
+    (dict(batch=1 << 20, n_q_heads=1 << 10, n_kv_heads=1 << 10), -22),
+])
+def test_append_invalid_shapes_rejected_on_host(host_lib, kw, code):
+    s = shape(host_lib, **kw)
+    L = host_lib.lib()
+    rc = L.kv_cache_append(16, 16, 16, 16, 16, 16, None, None, ctypes.byref(s), None)
+    assert rc == code
+    assert host_lib.last_error() != ""
+
+
+def test_append_bad_pointers_rejected_on_host(host_lib):
+    L = host_lib.lib()
+    s = shape(host_lib)
+    assert L.kv_cache_append(16, 16, 16, None, 16, 16, None, None, ctypes.byref(s), None) == -22   # null tensor
+    assert L.kv_cache_append(16, 16, 16, 16, 16, 18, None, None, ctypes.byref(s), None) == -22   # misaligned
+    one = (ctypes.c_float * 2)(1.0, 1.0)
+    assert L.kv_cache_append(16, 16, 16, 16, 16, 16, one, one, ctypes.byref(s), None) == -22     # scales on bf16
+    s8 = shape(host_lib, kv_fp8=True)
+    assert L.kv_cache_append(16, 16, 16, 16, 16, 16, None, None, ctypes.byref(s8), None) == -22  # fp8 without scales
+    assert L.kv_cache_append(None, None, None, None, None, None, None, None, None, None) == -22   # null shape
+    s0 = shape(host_lib, batch=0)
+    assert L.kv_cache_append(None, None, None, None, None, None, None, None, ctypes.byref(s0), None) == 0  # nothing to do
