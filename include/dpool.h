@@ -375,7 +375,7 @@ typedef struct {
   int32_t max_context_len;
   int32_t kv_dtype;   /* DP_KV_*                                             */
   int32_t out_dtype;  /* DP_OUT_*                                            */
-  int32_t query_tile; /* query tokens per workgroup: 0 or 32 (the only size) */
+  int32_t query_tile; /* query tokens per work item: 0 or 32 (the only size) */
   int32_t reserved;   /* must be 0                                           */
   int64_t total_q;    /* rows of q and out                                   */
   int64_t num_blocks; /* blocks in k_blocks / v_blocks                       */
