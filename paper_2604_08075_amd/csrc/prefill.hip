@@ -125,7 +125,7 @@ __device__ __forceinline__ int vpos(int row, int chunk) { return row * kVRow + (
 
 __device__ __forceinline__ uint16_t f32_to_bf16_bits(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
 
-// R: 16-token query column blocks per wave, so QT = 16 R query tokens per workgroup.
+// R: 16-token query column blocks per wave, so QT = 16 R query tokens per item.
 template <bool FP8, int R>
 __global__ __launch_bounds__(kWaves * 64, 1) void prefill_kernel(PrefillArgs a) {
   constexpr int QT = 16 * R;
@@ -540,7 +540,7 @@ extern "C" int chunked_prefill_attention(const void* q, const void* k_blocks, co
   constexpr int QT = 32;  // one eight-wave workgroup per compute unit, two waves per SIMD
   const int group = sh->n_q_heads / sh->n_kv_heads;
   const int nquad = (group + kWaves - 1) / kWaves;
-  // an upper bound of sum_s ceil(n_s / QT); surplus workgroups exit at once
+  // an upper bound of sum_s ceil(n_s / QT) items (the kernel counts them exactly)
   const int64_t tiles = (sh->total_q + QT - 1) / QT + sh->batch;
   const int64_t items = tiles * sh->n_kv_heads * nquad;
   if (items > INT32_MAX / 2) return fail(DP_EINVAL, "chunked_prefill_attention: too many query tiles");
