@@ -284,7 +284,7 @@ def main():
     ap.add_argument("--wgs-per-cu", type=int, default=0, help="resident workgroups per CU (0 = library choice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true", help="skip the chunked-prefill attention timing")
-    ap.add_argument("--prefill-tile", type=int, default=0, help="query tokens per prefill workgroup (0 or 32)")
+    ap.add_argument("--prefill-tile", type=int, default=0, help="query tokens per prefill work item (0 or 32)")
     ap.add_argument("--prefill-only", action="store_true", help="only time the chunked-prefill attention")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB 10 times (counter calibration) and exit")
