@@ -4,21 +4,29 @@
 One "step" is one decode step of one layer for the whole batch: one launch
 of the decode kernel, which streams every cached K and V element once and
 merges split-K partials inside the same launch - every stage of the hot
-path, with the inputs already resident in HBM.  Successive steps rotate over R independent copies
-of the layer's KV pool (R * KV bytes >= 1 GiB), so the 256 MB Infinity
-Cache cannot serve a step from the previous one.
+path, with the inputs already resident in HBM.  Successive steps rotate
+over R independent copies of the layer's KV pool (R * KV bytes >= 1 GiB),
+so the 256 MB Infinity Cache cannot serve a step from the previous one.
 
 The headline workload is the short pool (B=128, Llama-3-70B layer shape,
 bf16 KV, C_max 8192); the long pool (B=16, C_max 65536), the homogeneous
 pool (B=16, mixed lengths, C_max 65536) and the Qwen3-shaped fp8 short pool
 are reported beside it in the same line, as the metric compares the pools.
 Each pool also times the KV-cache append of its batch (one new token per
-sequence), and the line carries the paper's fleet cost model evaluated with
-the decode-attention throughput ratio measured here (context only).
+sequence).  The line also carries:
+  roofline      the decode kernel against 8 TB/s, with HBM traffic from the
+                committed rocprofv3 counter summary when it matches the source;
+  cpu_baseline  the fp64 oracle timed on this host over the same batch;
+  cost_model    the paper's fleet cost model with the throughput ratio
+                measured here (context only);
+  router        the host router's dispatch rate and one adaptive-threshold step;
+  chunked_prefill  the chunked-prefill attention on its two workloads, against
+                the dense bf16 MFMA peak.
 
 Output: one JSON line on stdout.  Progress goes to stderr.
 
-  python bench.py [--gpus 1] [--steps 100] [--warmup 10] [--configs 2,3,4,5] [--no-cpu-baseline]
+  python bench.py [--gpus 1] [--steps 100] [--warmup 10] [--config 2] [--configs 3,4,5]
+                  [--no-cpu-baseline] [--no-prefill] [--prefill-only]
 """
 from __future__ import annotations
 
