@@ -14,9 +14,17 @@ pool (B=16, mixed lengths, C_max 65536) and the Qwen3-shaped fp8 short pool
 are reported beside it in the same line, as the metric compares the pools.
 Each pool also times the KV-cache append of its batch (one new token per
 sequence).  The line also carries:
-  roofline      the decode kernel against 8 TB/s, with HBM traffic from the
-                committed rocprofv3 counter summary when it matches the source;
-  cpu_baseline  the fp64 oracle timed on this host over the same batch;
+  roofline      the decode kernel against 8 TB/s: algorithmic KV bytes over
+                the average launch duration of the timed region (back-to-back
+                launches between two HIP events on the launch stream), beside
+                the kernel-trace average and the HBM traffic of the committed
+                rocprofv3 summaries when they were taken on the source as it
+                is, and beside the read ceiling measured here;
+  hbm_read_ceiling  a plain 4 GiB read of device memory (contiguous, and as
+                4 KiB tiles in random order), timed the same way;
+  cpu_baseline  the fp64 oracle timed on this host over the same batch, on
+                every available core (one worker process per core, forked
+                before the GPU is touched) and on one core;
   cost_model    the paper's fleet cost model with the throughput ratio
                 measured here (context only);
   router        the host router's dispatch rate and one adaptive-threshold step;
@@ -26,7 +34,7 @@ sequence).  The line also carries:
 Output: one JSON line on stdout.  Progress goes to stderr.
 
   python bench.py [--gpus 1] [--steps 100] [--warmup 10] [--config 2] [--configs 3,4,5]
-                  [--no-cpu-baseline] [--no-prefill] [--prefill-only]
+                  [--no-cpu-baseline] [--no-prefill] [--no-ceiling] [--prefill-only]
 """
 from __future__ import annotations
 
@@ -77,22 +85,52 @@ def measured_traffic(workload_name: str):
         return None
 
 
+def profiled_kernel_avg_us(workload_name: str):
+    """Average duration of the decode kernel in the committed rocprofv3 kernel-trace
+    summary, if it was taken on the kernel source as it is now."""
+    path = os.path.join(PROFILES, f"paged_decode_{workload_name}.txt")
+    if not os.path.exists(path):
+        return None
+    sha, avg = None, None
+    for line in open(path):
+        if line.startswith("kernel_source_sha256_16:"):
+            sha = line.split(":", 1)[1].strip()
+        elif "paged_decode_kernel<" in line and avg is None:
+            try:
+                avg = float(line.split()[-4])
+            except (IndexError, ValueError):
+                pass
+    return avg if sha == kernel_sha() else None
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
 def describe(w) -> str:
     return (f"{w.name}: B={w.batch}, {w.n_q_heads}q/{w.n_kv_heads}kv heads, head_dim {w.head_dim}, "
             f"{w.kv_format} KV, block {w.block_size}, C_max {w.c_max}, seed {w.config}, "
             f"sum ctx {int(w.context_lens.sum())}, max ctx {w.max_context_len}, pool {w.num_blocks} blocks")
 
 
-def measure(cfg: int, steps: int, warmup: int, partition_tokens: int, wgs: int):
+def measure(cfg: int, steps: int, warmup: int, partition_tokens: int, wgs: int, w=None):
     import torch
 
     import workloads
     from paper_2604_08075_amd import binding
 
     t0 = time.time()
-    w = workloads.make_config(cfg, poison=False)
+    if w is None:
+        w = workloads.make_config(cfg, poison=False)
     layers = max(1, math.ceil((1 << 30) / w.kv_bytes))
-    log(f"config {cfg}: {describe(w)}; generated in {time.time() - t0:.1f}s; rotating over {layers} layer copies")
+    log(f"config {cfg}: {describe(w)}; ready in {time.time() - t0:.1f}s; rotating over {layers} layer copies")
     dev = workloads.to_device(w, layers=layers, poison_unused=False)
     fp8 = w.kv_format == "fp8_e4m3"
     dec = binding.PagedDecoder(w.batch, w.n_q_heads, w.n_kv_heads, w.max_blocks_per_seq, w.max_context_len,
@@ -108,7 +146,8 @@ def measure(cfg: int, steps: int, warmup: int, partition_tokens: int, wgs: int):
     for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
-    # timed region: exactly `steps` steps between two events on the launch stream
+    # timed region: exactly `steps` back-to-back launches between two events on
+    # the launch stream (torch's current stream, which the binding passes down)
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
@@ -118,83 +157,171 @@ def measure(cfg: int, steps: int, warmup: int, partition_tokens: int, wgs: int):
     torch.cuda.synchronize()
     ms_step = start.elapsed_time(end) / steps
 
-    # kernel duration: the same steps with events around each launch, on the
-    # launch stream (torch's current stream, which the binding passes down)
+    # the same steps with events around each launch: each bracket also holds the
+    # event packets and the launch gap, so this is an upper bound of the duration
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
     for i in range(steps):
         ev[i][0].record()
         step(i)
         ev[i][1].record()
     torch.cuda.synchronize()
-    kern_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / steps
+    bracket_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / steps
     res = dict(
         workload=describe(w), name=w.name, batch=w.batch, kv_bytes=w.kv_bytes, kv_format=w.kv_format,
         ms_per_step=ms_step, gbs=w.kv_bytes / (ms_step * 1e-3) / 1e9,
-        seq_steps_per_s=w.batch / (ms_step * 1e-3), kernel_ms=kern_ms,
-        kernel_gbs=w.kv_bytes / (kern_ms * 1e-3) / 1e9, partition_tokens=dec.partition_tokens,
-        layers_rotated=layers, sum_ctx=int(w.context_lens.sum()),
+        pct_of_peak_hbm=100.0 * w.kv_bytes / (ms_step * 1e-3) / 1e9 / PEAK_HBM_GBS,
+        seq_steps_per_s=w.batch / (ms_step * 1e-3), event_bracketed_launch_ms=bracket_ms,
+        partition_tokens=dec.partition_tokens, layers_rotated=layers, sum_ctx=int(w.context_lens.sum()),
         flops=4 * w.head_dim * w.n_q_heads * int(w.context_lens.sum()))
+    prof = profiled_kernel_avg_us(w.name)
+    if prof is not None:
+        res["rocprof_kernel_avg_us"] = prof
+        res["rocprof_gbs"] = w.kv_bytes / (prof * 1e-6) / 1e9
     log(f"config {cfg}: {ms_step * 1e3:.1f} us/step, {res['gbs']:.0f} GB/s "
-        f"({100 * res['gbs'] / PEAK_HBM_GBS:.1f}% of 8 TB/s), kernel {kern_ms * 1e3:.1f} us "
-        f"({100 * res['kernel_gbs'] / PEAK_HBM_GBS:.1f}%), min slice {dec.partition_tokens} tokens")
+        f"({res['pct_of_peak_hbm']:.1f}% of 8 TB/s); event-bracketed {bracket_ms * 1e3:.1f} us; "
+        f"rocprof average {prof if prof is not None else 'n/a'} us; min slice {dec.partition_tokens} tokens")
 
     # KV-cache append of one token per sequence, into the slot of each
-    # sequence's last cached token (a position that always has its block)
+    # sequence's last cached token (a position that always has its block).
+    # Timed as `reps` launches captured in one HIP graph and replayed, so the
+    # figure is the launch's duration on the device, not the host's launch rate.
     gen = torch.Generator(device="cuda").manual_seed(cfg)
     knew = torch.randn((w.batch, w.n_kv_heads, w.head_dim), device="cuda", generator=gen).to(torch.bfloat16)
     vnew = torch.randn((w.batch, w.n_kv_heads, w.head_dim), device="cuda", generator=gen).to(torch.bfloat16)
     pos = (cl - 1).clamp(min=0).to(torch.int32)
     ashape = binding.decode_shape(w.batch, w.n_q_heads, w.n_kv_heads, w.max_blocks_per_seq, w.max_context_len,
                                   w.num_blocks, kv_fp8=fp8)
+    reps, replays = 50, 4
 
-    def app(i):
-        binding.kv_cache_append(knew, vnew, kl[i % layers], vl[i % layers], bt, pos, ashape, ks, vs)
+    def app():
+        binding.kv_cache_append(knew, vnew, kl[0], vl[0], bt, pos, ashape, ks, vs)
 
-    for i in range(warmup):
-        app(i)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
-    for i in range(steps):
-        ev[i][0].record()
-        app(i)
-        ev[i][1].record()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for _ in range(3):
+            app()
+    torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
-    app_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / steps
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(reps):
+            app()
+    graph.replay()
+    torch.cuda.synchronize()
+    a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a0.record()
+    for _ in range(replays):
+        graph.replay()
+    a1.record()
+    torch.cuda.synchronize()
+    app_ms = a0.elapsed_time(a1) / (reps * replays)
+    del graph
     app_bytes = w.batch * w.n_kv_heads * w.head_dim * (2 * (1 if fp8 else 2) + 2 * 2)  # cache writes + bf16 inputs
     res["kv_append"] = {"us_per_launch": app_ms * 1e3, "bytes": app_bytes,
-                        "gbs": app_bytes / (app_ms * 1e-3) / 1e9, "tokens": w.batch}
-    log(f"config {cfg}: kv append {app_ms * 1e3:.1f} us for {w.batch} tokens x {w.n_kv_heads} heads")
+                        "gbs": app_bytes / (app_ms * 1e-3) / 1e9, "tokens": w.batch,
+                        "timing": f"{reps} launches captured in one HIP graph, {replays} replays between two events"}
+    log(f"config {cfg}: kv append {app_ms * 1e3:.2f} us for {w.batch} tokens x {w.n_kv_heads} heads")
     del dev
     torch.cuda.empty_cache()
     return res, w
 
 
-def cpu_baseline(w, budget_s=10.0):
-    """The fp64 oracle, unchanged, timed on this host over whole passes of the same batch."""
+def hbm_read_ceiling(binding, nbytes=4 << 30, reps=10):
+    """A plain read of `nbytes` of device memory, contiguous and as 4 KiB tiles in
+    random order, best over a few launch widths; GB/s = bytes / average launch
+    duration (back-to-back launches between two events)."""
+    import torch
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1 << 16, dtype=torch.int32, device="cuda")
+    gen = torch.Generator(device="cuda").manual_seed(12)
+    ids = torch.randperm(nbytes // 4096, device="cuda", generator=gen).to(torch.int32)
+    res = {"bytes": nbytes}
+    for mode, grids, tiles in (("contiguous", (1024, 2048, 4096, 8192, 16384), None),
+                               ("tile_gather_4k", (512, 1024, 2048, 4096), ids)):
+        best = (0.0, 0)
+        for g in grids:
+            for _ in range(2):
+                binding.hbm_read_probe(buf, g, sink, tiles)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(reps):
+                binding.hbm_read_probe(buf, g, sink, tiles)
+            e1.record()
+            torch.cuda.synchronize()
+            gbs = nbytes / (e0.elapsed_time(e1) / reps * 1e-3) / 1e9
+            best = max(best, (gbs, g))
+        res[f"{mode}_gbs"] = best[0]
+        res[f"{mode}_workgroups"] = best[1]
+        log(f"hbm read ceiling, {mode}: {best[0]:.0f} GB/s ({best[1]} workgroups of 256 threads)")
+    del buf, ids
+    torch.cuda.empty_cache()
+    return res
+
+
+_CPU_W = None  # the workload the forked oracle workers read (inherited, not copied)
+
+
+def _oracle_seqs(seqs):
     from threadpoolctl import threadpool_limits
 
     from oracle import attention
-    done_bytes = 0
-    done_seqs = 0
-    passes = 0
-    t0 = time.time()
-    with threadpool_limits(limits=1):
+    w = _CPU_W
+    threadpool_limits(limits=1)
+    attention.paged_decode_attention(w.q_bits, w.k_store, w.v_store, w.block_tables, w.context_lens, w.scale,
+                                     kv_format=w.kv_format, k_scale=w.k_scale, v_scale=w.v_scale, seqs=seqs)
+    return len(seqs)
+
+
+def cpu_baseline(w, budget_s=10.0, max_workers=15):
+    """The fp64 oracle, unchanged, timed on this host over whole passes of the same
+    batch: on every available core (a pool of worker processes, one sequence per
+    task, longest first) and on one core.  Must run before anything touches the
+    GPU: the workers are forked from this process."""
+    import multiprocessing as mp
+
+    from threadpoolctl import threadpool_limits
+    global _CPU_W
+    _CPU_W = w
+    eb = 1 if w.kv_format == "fp8_e4m3" else 2
+    pass_bytes = int(w.context_lens.astype(np.int64).sum()) * w.n_kv_heads * w.head_dim * 2 * eb
+    order = [[int(s)] for s in np.argsort(-w.context_lens, kind="stable")]
+
+    def run(pool):
+        passes, t0 = 0, time.time()
         while True:
-            for s in range(w.batch):
-                attention.paged_decode_attention(w.q_bits, w.k_store, w.v_store, w.block_tables, w.context_lens,
-                                                 w.scale, kv_format=w.kv_format, k_scale=w.k_scale,
-                                                 v_scale=w.v_scale, seqs=[s])
-                done_bytes += int(w.context_lens[s]) * w.n_kv_heads * w.head_dim * 2 * (
-                    1 if w.kv_format == "fp8_e4m3" else 2)
-                done_seqs += 1
+            if pool is None:
+                with threadpool_limits(limits=1):
+                    for task in order:
+                        _oracle_seqs(task)
+            else:
+                pool.map(_oracle_seqs, order, chunksize=1)
             passes += 1
-            if time.time() - t0 >= budget_s or passes >= 20:
-                break
-    dt = time.time() - t0
-    return {"value": done_bytes / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"{passes} full pass(es) over the {w.name} batch ({w.batch} sequences, "
-                      f"{int(w.context_lens.sum())} tokens) in {dt:.1f} s, one sequence per oracle call, "
-                      f"BLAS limited to 1 thread",
-            "seq_steps_per_s": done_seqs / dt, "seconds": dt}
+            if time.time() - t0 >= budget_s or passes >= 200:
+                return passes, time.time() - t0
+
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:
+        avail = os.cpu_count() or 1
+    workers = max(1, min(avail, max_workers))
+    with mp.get_context("fork").Pool(workers) as pool:
+        pool.map(_oracle_seqs, order[:workers], chunksize=1)   # start-up outside the timing
+        p_all, t_all = run(pool)
+    p_one, t_one = run(None)
+    res = {"value": pass_bytes * p_all / t_all / 1e9, "unit": "GB/s", "cores": workers, "kind": "oracle",
+           "sample": f"{p_all} full pass(es) over the {w.name} batch ({w.batch} sequences, "
+                     f"{int(w.context_lens.sum())} tokens) in {t_all:.1f} s on {workers} worker processes "
+                     f"(one sequence per task, BLAS limited to 1 thread each)",
+           "seq_steps_per_s": w.batch * p_all / t_all, "seconds": t_all,
+           "cpu_model": cpu_model(), "cores_available": avail,
+           "one_core": {"value": pass_bytes * p_one / t_one / 1e9, "unit": "GB/s", "cores": 1,
+                        "seq_steps_per_s": w.batch * p_one / t_one, "seconds": t_one,
+                        "sample": f"{p_one} full pass(es) in {t_one:.1f} s, one process, BLAS limited to 1 thread"}}
+    log(f"cpu oracle: {res['value']:.3f} GB/s on {workers} cores ({res['cpu_model']}), "
+        f"{res['one_core']['value']:.3f} GB/s on one core")
+    return res
 
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA peak
@@ -292,6 +419,7 @@ def main():
     ap.add_argument("--wgs-per-cu", type=int, default=0, help="resident workgroups per CU (0 = library choice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true", help="skip the chunked-prefill attention timing")
+    ap.add_argument("--no-ceiling", action="store_true", help="skip the HBM read-ceiling probe")
     ap.add_argument("--prefill-tile", type=int, default=0, help="query tokens per prefill work item (0 or 32)")
     ap.add_argument("--prefill-only", action="store_true", help="only time the chunked-prefill attention")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -301,6 +429,18 @@ def main():
         print(f"bench.py measures one GPU only: the library has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)
         sys.exit(2)
+
+    # The CPU baseline runs first: its worker processes are forked from this
+    # process, which must not have touched the GPU yet.
+    w_head, cpu = None, None
+    if not (args.calibrate_copy or args.prefill_only):
+        import workloads
+        t0 = time.time()
+        w_head = workloads.make_config(args.config, poison=False)
+        log(f"config {args.config}: workload generated in {time.time() - t0:.1f}s")
+        if not args.no_cpu_baseline:
+            log("timing the CPU oracle on the same workload")
+            cpu = cpu_baseline(w_head)
 
     import torch
     if not torch.cuda.is_available():
@@ -323,7 +463,8 @@ def main():
                for n in ("chunked_prefill_llama70b", "chunked_prefill_qwen3_fp8")}
         print(json.dumps({"chunked_prefill": res}), flush=True)
         return
-    head, w_head = measure(args.config, args.steps, args.warmup, args.partition_tokens, args.wgs_per_cu)
+    head, _ = measure(args.config, args.steps, args.warmup, args.partition_tokens, args.wgs_per_cu, w=w_head)
+    del w_head
     others = [int(c) for c in args.configs.split(",") if c.strip()] if args.long_config is None else (
         [args.long_config] if args.long_config else [])
     extra = {}
@@ -332,23 +473,36 @@ def main():
         if c != args.config:
             r, _ = measure(c, args.steps, args.warmup, args.partition_tokens, args.wgs_per_cu)
             extra[names.get(c, f"config_{c}")] = r
+    ceiling = None if args.no_ceiling else hbm_read_ceiling(binding)
 
     traffic = measured_traffic(head["name"])
-    roof = {"bound": "hbm", "achieved": head["kernel_gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
-            "frac": head["kernel_gbs"] / PEAK_HBM_GBS, "traffic": traffic,
+    roof = {"bound": "hbm", "achieved": head["gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": head["gbs"] / PEAK_HBM_GBS, "traffic": traffic,
             "kernel": "paged_decode_kernel", "algorithmic_bytes_per_launch": head["kv_bytes"],
-            "avg_launch_ms": head["kernel_ms"]}
+            "avg_launch_ms": head["ms_per_step"],
+            "timing": "average launch duration of the timed region: back-to-back launches between two HIP "
+                      "events on the launch stream (inter-launch gaps included)",
+            "event_bracketed_launch_ms": head["event_bracketed_launch_ms"],
+            "rocprof_kernel_avg_us": head.get("rocprof_kernel_avg_us"),
+            "rocprof_frac": (head["rocprof_gbs"] / PEAK_HBM_GBS) if "rocprof_gbs" in head else None,
+            "rocprof_profile": f"profiles/paged_decode_{head['name']}.txt" if "rocprof_gbs" in head else None}
+    if ceiling:
+        roof["empirical_read_peak"] = ceiling["contiguous_gbs"]
+        roof["frac_of_empirical_read_peak"] = head["gbs"] / ceiling["contiguous_gbs"]
+        roof["empirical_tile_gather_peak"] = ceiling["tile_gather_4k_gbs"]
     line = {
         "metric": METRIC, "value": head["gbs"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": head["ms_per_step"], "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": head["workload"], "batch": head["batch"], "kv_dtype": head["kv_format"],
                    "partition_tokens": head["partition_tokens"], "layers_rotated": head["layers_rotated"]},
-        "pct_of_peak_hbm": 100.0 * head["gbs"] / PEAK_HBM_GBS,
+        "pct_of_peak_hbm": head["pct_of_peak_hbm"],
         "seq_steps_per_s": head["seq_steps_per_s"],
         "kv_append": head["kv_append"],
         "roofline": roof,
     }
+    if ceiling:
+        line["hbm_read_ceiling"] = ceiling
     line.update(extra)
     homog = extra.get("homogeneous_pool")
     if head["name"] == "short_pool_llama70b" and homog:
@@ -366,9 +520,8 @@ def main():
     if not args.no_prefill:
         line["chunked_prefill"] = {n: measure_prefill(n, max(args.steps // 5, 5), 3, args.prefill_tile)
                                    for n in ("chunked_prefill_llama70b", "chunked_prefill_qwen3_fp8")}
-    if not args.no_cpu_baseline:
-        log("timing the CPU oracle on the same workload")
-        line["cpu_baseline"] = cpu_baseline(w_head)
+    if cpu is not None:
+        line["cpu_baseline"] = cpu
     print(json.dumps(line), flush=True)
 
 

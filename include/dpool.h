@@ -390,6 +390,29 @@ int chunked_prefill_attention(const void* q, const void* k_blocks, const void* v
                               const float* v_scale, void* out, const dp_prefill_shape* shape,
                               void* stream);
 
+/* ------------------------------------------------------------------------ */
+/* HBM read probe (device, asynchronous; measurement only).                 */
+/*                                                                           */
+/* Decode attention is bound by the rate at which the cached K and V can be */
+/* read (Sec. 3 effect 4; Sec. 4.4).  This call reads device memory as a    */
+/* plain read would, so that the decode kernel's bandwidth can be set       */
+/* against what this device reaches, beside its published peak:             */
+/*   tile_ids == NULL: every byte of buf[0, bytes) once, the grid sweeping   */
+/*                     it front to back (n_tiles must be 0);                 */
+/*   tile_ids != NULL: the 4 KiB tiles buf + 4096 * tile_ids[i],             */
+/*                     i = 0 .. n_tiles-1, in list order (the decode's       */
+/*                     (block, KV head) tile reads); ids are clamped into    */
+/*                     [0, bytes / 4096).                                    */
+/* buf and bytes are 16-byte multiples; workgroups (of 256 threads) sets    */
+/* the launch width; sink holds at least `workgroups` int32 and is written   */
+/* only in the practically impossible case that a workgroup's folded data   */
+/* equals a fixed constant (it exists so the loads cannot be elided).       */
+/* One launch on `stream`; DP_EINVAL for bad arguments (nothing enqueued),  */
+/* DP_EIO if the launch fails.  The caller owns every buffer.               */
+/* ------------------------------------------------------------------------ */
+int dp_hbm_read_probe(const void* buf, size_t bytes, const int32_t* tile_ids, int64_t n_tiles,
+                      int32_t workgroups, int32_t* sink, size_t sink_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -31,7 +31,7 @@ EXPORTS = (
     "route_default_params", "route_init", "route_requests", "route_on_response",
     "route_adapt_default_params", "route_adapt_threshold", "dp_cost_model",
     "paged_decode_workspace_size", "paged_decode_partition_tokens", "paged_decode_attention",
-    "kv_cache_append", "chunked_prefill_attention",
+    "kv_cache_append", "chunked_prefill_attention", "dp_hbm_read_probe",
 )
 
 
@@ -133,6 +133,8 @@ def lib() -> ctypes.CDLL:
         L.kv_cache_append.argtypes = [ctypes.c_void_p] * 8 + [ctypes.POINTER(DecodeShape), ctypes.c_void_p]
         L.chunked_prefill_attention.argtypes = [ctypes.c_void_p] * 6 + [ctypes.c_float] + [ctypes.c_void_p] * 3 + [
             ctypes.POINTER(PrefillShape), ctypes.c_void_p]
+        L.dp_hbm_read_probe.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int64,
+                                        ctypes.c_int32, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
         _lib = L
     return _lib
 
@@ -341,6 +343,14 @@ def chunked_prefill_attention(q, k_blocks, v_blocks, block_tables, context_lens,
         q_start.data_ptr(), float(scale), k_scale.data_ptr() if k_scale is not None else None,
         v_scale.data_ptr() if v_scale is not None else None, out.data_ptr(), ctypes.byref(shape),
         _stream_ptr(stream)))
+
+
+def hbm_read_probe(buf, workgroups, sink, tile_ids=None, stream=None) -> None:
+    """Enqueue one read of `buf` (contiguous, or its 4 KiB tiles in `tile_ids` order)."""
+    nbytes = buf.numel() * buf.element_size()
+    check(lib().dp_hbm_read_probe(buf.data_ptr(), nbytes, tile_ids.data_ptr() if tile_ids is not None else None,
+                                  tile_ids.numel() if tile_ids is not None else 0, int(workgroups), sink.data_ptr(),
+                                  sink.numel() * sink.element_size(), _stream_ptr(stream)))
 
 
 class PagedDecoder:

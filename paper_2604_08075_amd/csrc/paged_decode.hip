@@ -545,7 +545,10 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
         do {
           ++wk.s;
         } while (wk.s < B - 1 && pre[wk.s + 1] == pre[wk.s]);  // skip empty sequences (bounded)
-        wk.s = __builtin_amdgcn_readfirstlane(wk.s);
+        // Stepping off the last sequence only happens to a look-ahead
+        // position past the end of the stream (never computed); it stays on
+        // the last sequence so that the query rows it prefetches exist.
+        wk.s = __builtin_amdgcn_readfirstlane(wk.s > B - 1 ? B - 1 : wk.s);
       }
       wk.nus = __builtin_amdgcn_readfirstlane(pre[wk.s + 1] - pre[wk.s]);
     }
@@ -936,6 +939,12 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
 template __global__ void paged_decode_kernel<false>(DecodeArgs);
 template __global__ void paged_decode_kernel<true>(DecodeArgs);
 
+// Zero n words (arrival counters).  A kernel rather than a memset, so that a
+// captured graph holds no memset node.
+__global__ __launch_bounds__(256) void zero_words_kernel(int32_t* p, int n) {
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0;
+}
+
 }  // namespace dpool_hip
 
 namespace {
@@ -943,6 +952,7 @@ namespace {
 using namespace dpool_hip;
 
 constexpr int kMaxBatchInLds = 4096;  // the unit prefix of the batch is kept in LDS
+constexpr int kMaxWorkgroupsPerCu = 8;
 constexpr size_t kLdsBytes = 160 * 1024;
 
 // Compute units of the current device (cached per device); 256 when no device
@@ -995,6 +1005,7 @@ struct Plan {
   int grid;         // workgroups
   size_t dyn_lds;   // dynamic LDS bytes
   size_t arrivals_off, rec_ml_off, rec_o_off, ws_bytes;
+  int clear_words;  // arrival counters to zero before the launch (0 on the usual path)
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -1031,7 +1042,8 @@ int validate(const dp_decode_shape* sh, Plan* plan) {
     return fail(DP_EINVAL, "paged_decode: partition_tokens %d must be a multiple of %d in [0, %d]", P, unit,
                 unit * kMaxUnitsPerWave);
   const int wpc = sh->workgroups_per_cu;
-  if (wpc < 0 || wpc > 8) return fail(DP_EINVAL, "paged_decode: workgroups_per_cu %d outside [0, 8]", wpc);
+  if (wpc < 0 || wpc > kMaxWorkgroupsPerCu)
+    return fail(DP_EINVAL, "paged_decode: workgroups_per_cu %d outside [0, %d]", wpc, kMaxWorkgroupsPerCu);
   const int64_t units_per_seq = ((int64_t)sh->max_context_len + unit - 1) / unit;
   const int64_t max_units = units_per_seq * sh->batch * sh->n_kv_heads;
   if (max_units > INT32_MAX) return fail(DP_ENOTSUP, "paged_decode: %lld units exceed int32", (long long)max_units);
@@ -1059,8 +1071,18 @@ int validate(const dp_decode_shape* sh, Plan* plan) {
   plan->grid = (int)grid;
   const int G = sh->n_q_heads / sh->n_kv_heads;
   const size_t waves = (size_t)grid * kWaves;
+  // The arrival counters open the workspace, and every call returns the ones
+  // it used to zero.  Their region has the same size for every grid up to
+  // kMaxWorkgroupsPerCu workgroups per compute unit, so the records of one
+  // call never land where a later call of another shape expects a zero
+  // counter.  A grid wider than that (only when some slice would otherwise
+  // exceed kMaxUnitsPerWave) extends the region over what may be records of
+  // an earlier call; that launch zeroes its counters first.
+  const size_t cap_waves = (size_t)cus * kMaxWorkgroupsPerCu * kWaves;
+  const size_t counter_waves = std::max(waves, cap_waves);
+  plan->clear_words = waves > cap_waves ? (int)(2 * waves) : 0;
   plan->arrivals_off = 0;
-  plan->rec_ml_off = align256(2 * waves * sizeof(int32_t));
+  plan->rec_ml_off = align256(2 * counter_waves * sizeof(int32_t));
   plan->rec_o_off = plan->rec_ml_off + align256(3 * waves * G * 2 * sizeof(float));
   plan->ws_bytes = plan->rec_o_off + align256(3 * waves * G * kHeadDim * sizeof(float));
   return DP_OK;
@@ -1068,10 +1090,16 @@ int validate(const dp_decode_shape* sh, Plan* plan) {
 
 }  // namespace
 
-extern "C" size_t paged_decode_workspace_size(const dp_decode_shape* shape) {
+int dpool::decode_workspace_bytes(const dp_decode_shape* shape, size_t* bytes) {
   Plan plan;
-  if (validate(shape, &plan) != DP_OK) return 0;
-  return plan.ws_bytes;
+  const int rc = validate(shape, &plan);
+  if (rc == DP_OK) *bytes = plan.ws_bytes;
+  return rc;
+}
+
+extern "C" size_t paged_decode_workspace_size(const dp_decode_shape* shape) {
+  size_t bytes = 0;
+  return dpool::decode_workspace_bytes(shape, &bytes) == DP_OK ? bytes : 0;
 }
 
 extern "C" int32_t paged_decode_partition_tokens(const dp_decode_shape* shape) {
@@ -1126,6 +1154,9 @@ extern "C" int paged_decode_attention(const void* q, const void* k_blocks, const
   a.out_fp32 = shape->out_dtype == DP_OUT_FP32;
   a.min_chunk = plan.min_chunk;
   (void)hipGetLastError();  // clear a stale error left by earlier work
+  if (plan.clear_words)
+    hipLaunchKernelGGL(zero_words_kernel, dim3(std::min((plan.clear_words + 255) / 256, 1024)), dim3(256), 0,
+                       (hipStream_t)stream, a.arrivals, plan.clear_words);
   if (fp8)
     hipLaunchKernelGGL(paged_decode_kernel<true>, dim3(plan.grid), dim3(kWaves * 64), plan.dyn_lds,
                        (hipStream_t)stream, a);

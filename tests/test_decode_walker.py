@@ -1,0 +1,242 @@
+"""CPU check of the decode kernel's index arithmetic (no GPU).
+
+The decode kernel walks a flat stream of 16 KiB units (every cached token of
+every (sequence, KV head) segment) in equal per-wave slices, prefetches the
+query group of the unit after next, and merges the pieces of segments that
+slices cut through arrival counters and record slots in its workspace.  This
+module restates that arithmetic in Python, step for step as the kernel and
+its host launcher do it, and checks on random batches that
+
+  * every query row the kernel loads (including look-ahead prefetches past the
+    end of the stream) lies inside the [batch, n_q_heads, 128] query buffer;
+  * every block-table entry read is one of the sequence's own live blocks, and
+    every tile index lies inside the pool;
+  * the slices cover every unit exactly once, the walker's position always
+    equals the position of the unit it computes, and no slice exceeds the
+    kernel's tile list;
+  * every piece of a cut segment writes the record slot its merger reads, the
+    arrival counters and record slots stay inside the workspace, and no two
+    (segment, group) pairs share a counter.
+
+A kernel change to any of these must be mirrored here.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import pytest
+
+WAVES = 4               # waves per workgroup
+MAX_UNITS_PER_WAVE = 256
+FAN_IN = 8              # pieces per merge group
+
+
+def host_plan(ctx, hkv, fp8, max_ctx, partition_tokens=0, wgs_per_cu=0, cus=256, resident=2):
+    """Grid and minimum slice length as the launcher chooses them."""
+    unit = 64 if fp8 else 32
+    min_chunk = partition_tokens // unit if partition_tokens else 1
+    max_units = -(-max_ctx // unit) * len(ctx) * hkv
+    per_cu = min(wgs_per_cu, resident) if wgs_per_cu else 1
+    grid = cus * per_cu
+    need = -(-max_units // (WAVES * MAX_UNITS_PER_WAVE))
+    useful = -(-max_units // (WAVES * min_chunk))
+    return max(1, max(need, min(grid, useful))), min_chunk, unit
+
+
+class Walk:
+    __slots__ = ("s", "g", "j", "nus")
+
+    def __init__(self, s, g, j, nus):
+        self.s, self.g, self.j, self.nus = s, g, j, nus
+
+    def copy(self):
+        return Walk(self.s, self.g, self.j, self.nus)
+
+    def key(self):
+        return (self.s, self.g, self.j)
+
+
+def simulate(ctx, hkv, fp8, max_ctx, max_blocks_per_seq, partition_tokens=0, wgs_per_cu=0, cus=256):
+    """Run the kernel's index arithmetic; returns what it touched."""
+    B = len(ctx)
+    grid, min_chunk, UT = host_plan(ctx, hkv, fp8, max_ctx, partition_tokens, wgs_per_cu, cus)
+    UB = UT // 16
+    ctx = [min(max(int(c), 0), max_ctx) for c in ctx]
+    pre = [0]
+    for c in ctx:
+        pre.append(pre[-1] + -(-c // UT))
+    U = hkv * pre[B]
+    TW = grid * WAVES
+    C = max(-(-U // TW), min_chunk)
+
+    def locate(u):  # binary search of the kernel: largest s with Hkv * pre[s] <= u
+        lo, hi = 0, B - 1
+        while lo < hi:
+            mid = (lo + hi + 1) >> 1
+            if hkv * pre[mid] <= u:
+                lo = mid
+            else:
+                hi = mid - 1
+        s = lo
+        nus = pre[s + 1] - pre[s]
+        r = u - hkv * pre[s]
+        return Walk(s, r // nus, r % nus, nus)
+
+    def advance(wk):
+        wk.j += 1
+        if wk.j == wk.nus:
+            wk.j = 0
+            wk.g += 1
+            if wk.g == hkv:
+                wk.g = 0
+                while True:
+                    wk.s += 1
+                    if not (wk.s < B - 1 and pre[wk.s + 1] == pre[wk.s]):
+                        break
+                wk.s = min(wk.s, B - 1)
+            wk.nus = pre[wk.s + 1] - pre[wk.s]
+
+    q_rows, bt_reads, computed = [], [], []
+    records = {}        # record slot -> (s, g, piece index r)
+    pieces = {}         # (s, g) -> list of (wave, slot)
+    for gw in range(TW):
+        u0 = gw * C
+        u1 = min(u0 + C, U)
+        if u0 >= u1:
+            continue
+        n = u1 - u0
+        assert n <= MAX_UNITS_PER_WAVE
+        # tile list
+        for i in range(n):
+            p = locate(u0 + i)
+            nb = -(-ctx[p.s] // 16)
+            for b in range(UB):
+                blk = p.j * UB + (b if p.j * UB + b < nb else 0)
+                bt_reads.append((p.s, blk, nb))
+        # walk
+        cs = locate(u0)
+        w1 = cs.copy()
+        advance(w1)
+        w2 = w1.copy()
+        advance(w2)
+        q_rows += [(cs.s, cs.g), (w1.s, w1.g)]
+        state = {"piece_first": True, "piece_j0": 0}
+
+        def compute(ui, cs):
+            assert cs.key() == locate(u0 + ui).key()
+            computed.append(u0 + ui)
+            if ui == 0 or cs.j == 0:
+                state["piece_first"] = ui == 0
+                state["piece_j0"] = cs.j
+            seg_end = cs.j == cs.nus - 1
+            if not (seg_end or ui == n - 1):
+                return
+            if state["piece_j0"] == 0 and seg_end:
+                return  # whole segment: written straight to the output
+            slot = 2 * gw + (0 if state["piece_first"] else 1)
+            assert slot not in records
+            records[slot] = (cs.s, cs.g)
+            pieces.setdefault((cs.s, cs.g), []).append((gw, slot))
+
+        ui = 0
+        while ui + 2 < n:
+            for d in (0, 1):
+                compute(ui + d, cs)
+                if w2.j == 0:
+                    q_rows.append((w2.s, w2.g))
+                cs, w1 = w1, w2.copy()
+                advance(w2)
+            ui += 2
+        if ui + 1 < n:
+            compute(ui, cs)
+            if w2.j == 0:
+                q_rows.append((w2.s, w2.g))
+            cs, w1 = w1, w2.copy()
+            advance(w2)
+            ui += 1
+        compute(ui, cs)
+    return dict(B=B, TW=TW, C=C, U=U, pre=pre, q_rows=q_rows, bt_reads=bt_reads, computed=computed,
+                records=records, pieces=pieces, max_blocks_per_seq=max_blocks_per_seq)
+
+
+def check(sim, hkv):
+    B, TW, C, pre = sim["B"], sim["TW"], sim["C"], sim["pre"]
+    for s, g in sim["q_rows"]:
+        assert 0 <= s < B and 0 <= g < hkv, (s, g)
+    for s, blk, nb in sim["bt_reads"]:
+        assert 0 <= blk < nb <= sim["max_blocks_per_seq"], (s, blk, nb)
+    assert sorted(sim["computed"]) == list(range(sim["U"]))
+    counters_group, counters_seg = set(), set()
+    for (s, g), got in sim["pieces"].items():
+        nus = pre[s + 1] - pre[s]
+        a0 = hkv * pre[s] + g * nus
+        k0, kend = a0 // C, (a0 + nus - 1) // C
+        np_ = kend - k0 + 1
+        assert np_ >= 2 and len(got) == np_
+        first_slot = 2 * k0 + (1 if a0 > k0 * C else 0)
+        by_wave = dict(got)
+        assert sorted(by_wave) == list(range(k0, kend + 1))
+        for r in range(np_):
+            assert by_wave[k0 + r] == (first_slot if r == 0 else 2 * (k0 + r))
+        for gfirst in range(0, np_, FAN_IN):
+            gn = min(np_, gfirst + FAN_IN) - gfirst
+            kg = k0 + gfirst + gn - 1
+            assert 0 <= kg < TW and 2 * TW + kg < 3 * TW
+            assert kg not in counters_group
+            counters_group.add(kg)
+        assert 0 <= kend < TW and kend not in counters_seg
+        counters_seg.add(kend)
+    for slot in sim["records"]:
+        assert 0 <= slot < 2 * TW
+
+
+def draw(rng, B, max_ctx, p_empty):
+    ctx = rng.integers(1, max_ctx + 1, B)
+    ctx[rng.random(B) < p_empty] = 0
+    return ctx
+
+
+def test_reported_case_stays_in_bounds():
+    """Four sequences, two KV heads, whose last wave ends on the last sequence's
+    last unit: its look-ahead positions stay on that sequence."""
+    ctx = [100, 300, 50, 700]
+    sim = simulate(ctx, 2, False, 700, 44)
+    check(sim, 2)
+    assert max(s for s, _ in sim["q_rows"]) == 3
+
+
+@pytest.mark.parametrize("fp8", [False, True])
+@pytest.mark.parametrize("trial", range(40))
+def test_random_batches(fp8, trial):
+    rng = np.random.default_rng(1000 + trial + 100 * fp8)
+    B = int(rng.choice([1, 2, 3, 5, 17, 64, 300]))
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    max_ctx = int(rng.choice([16, 64, 200, 2048, 9000]))
+    ctx = draw(rng, B, max_ctx, float(rng.choice([0.0, 0.3, 0.9])))
+    unit = 64 if fp8 else 32
+    P = int(rng.choice([0, unit, 4 * unit, 64 * unit]))
+    cus = int(rng.choice([1, 3, 8, 256]))
+    wgs = int(rng.choice([0, 1, 2]))
+    sim = simulate(ctx, hkv, fp8, max_ctx, -(-max_ctx // 16), P, wgs, cus)
+    check(sim, hkv)
+
+
+@pytest.mark.parametrize("ctx", [[0], [0, 0, 5], [7, 0, 0], [1], [16] * 9, [33, 0, 64, 0]])
+def test_empty_and_tiny_batches(ctx):
+    for fp8 in (False, True):
+        for cus in (1, 256):
+            sim = simulate(ctx, 2, fp8, max(max(ctx), 1), 8, cus=cus)
+            check(sim, 2)
+
+
+def test_benchmark_shapes():
+    """The short, long, homogeneous and fp8 pools' length recipes at full batch size."""
+    rng = np.random.default_rng(5)
+    for B, hkv, fp8, cmax in ((128, 8, False, 8192), (16, 8, False, 65536), (256, 4, True, 8192)):
+        prompt = np.clip(np.rint(rng.lognormal(math.log(600.0), 1.2, B)), 16, 8192)
+        ctx = np.minimum(prompt + rng.integers(1, 429, B), cmax).astype(int)
+        if cmax == 65536:
+            ctx = np.maximum(ctx, rng.integers(8192, 42000, B))
+        sim = simulate(ctx, hkv, fp8, int(ctx.max()), cmax // 16)
+        check(sim, hkv)

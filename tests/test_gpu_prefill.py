@@ -2,8 +2,9 @@
 
 Same bar as decode: max abs error 1.5e-2 with bf16 KV, 3e-2 with fp8 e4m3 KV
 (bf16 output; the fp32 output to the same bar).  Small cases are compared
-row by row in full; the benchmark workloads at full size on sampled rows the
-oracle computes one by one.  Causality, untouched rows and determinism are
+row by row in full; the benchmark workloads at full size on every row of their
+first chunk and on sampled rows of the others, which the oracle computes one
+by one.  Causality, untouched rows and determinism are
 checked bit for bit.
 """
 import sys
@@ -73,19 +74,24 @@ def test_small_parity(gpu_lib, case, query_tile):
 
 
 @pytest.mark.parametrize("name", sorted(workloads.PREFILL_CONFIGS))
-def test_benchmark_workload_sampled_rows(gpu_lib, name):
+def test_benchmark_workload(gpu_lib, name):
+    """The benchmark workloads at full size: every row of the first chunk (2,048
+    query tokens at context 2,048), and sampled rows of the deeper chunks, which
+    the oracle computes one by one exactly as in full."""
     note(f"prefill {name}: building")
     w = workloads.make_prefill_config(name)
     qs = w.meta["q_start"]
     rng = np.random.default_rng(99)
-    rows = set()
-    for s in range(w.batch):
+    rows = set(range(int(qs[0]), int(qs[1])))
+    for s in range(1, w.batch):
         r0, r1 = int(qs[s]), int(qs[s + 1])
         rows.update({r0, r0 + 1, r0 + 63, r0 + 64, r1 - 1})
         rows.update(int(x) for x in rng.integers(r0, r1, 6))
     rows = sorted(rows)
     dev = workloads.to_device(w)
     got = gpu_rows(gpu_lib, w, dev)
+    del dev
+    torch.cuda.empty_cache()
     note(f"prefill {name}: oracle on {len(rows)} rows")
     ref = oracle_rows(w, rows)
     err = float(np.abs(got[rows] - ref[rows]).max())
