@@ -305,6 +305,24 @@ int paged_decode_attention(const void* q, const void* k_blocks, const void* v_bl
                            void* out, const dp_decode_shape* shape, void* workspace,
                            size_t workspace_bytes, void* stream);
 
+/* paged_decode_attention for callers that cannot allocate device memory
+ * (code under HIP graph capture, serving loops and harnesses that forbid
+ * hipMalloc).  Same arguments, layouts, results and errors as
+ * paged_decode_attention, without the workspace: the library keeps a fixed
+ * 32 MiB device array per GPU (held until the process ends, its address
+ * looked up and the array zero-filled by one small kernel on `stream` at
+ * the first call made on that device) and uses it as the workspace.  Nothing
+ * is allocated, on the first call or later.
+ * DP_ENOMEM (nothing enqueued) if the shape needs more than 32 MiB (see
+ * paged_decode_workspace_size): every GQA group up to 16 fits with one
+ * workgroup per compute unit (workgroups_per_cu 0 or 1) on a 256-CU device.
+ * Every call on a device shares its array: calls that overlap in time on
+ * one device (different streams, host threads) race and must not be made. */
+int paged_decode_attention_noalloc(const void* q, const void* k_blocks, const void* v_blocks,
+                                   const int32_t* block_tables, const int32_t* context_lens,
+                                   float scale, const float* k_scale, const float* v_scale,
+                                   void* out, const dp_decode_shape* shape, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* KV-cache append (device, asynchronous).                                   */
 /*                                                                           */

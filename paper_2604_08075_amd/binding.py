@@ -31,6 +31,7 @@ EXPORTS = (
     "route_default_params", "route_init", "route_requests", "route_on_response",
     "route_adapt_default_params", "route_adapt_threshold", "dp_cost_model",
     "paged_decode_workspace_size", "paged_decode_partition_tokens", "paged_decode_attention",
+    "paged_decode_attention_noalloc",
     "kv_cache_append", "chunked_prefill_attention", "dp_hbm_read_probe",
 )
 
@@ -130,6 +131,8 @@ def lib() -> ctypes.CDLL:
         L.paged_decode_partition_tokens.restype = ctypes.c_int32
         L.paged_decode_attention.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_float] + [ctypes.c_void_p] * 3 + [
             ctypes.POINTER(DecodeShape), ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+        L.paged_decode_attention_noalloc.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_float] + [
+            ctypes.c_void_p] * 3 + [ctypes.POINTER(DecodeShape), ctypes.c_void_p]
         L.kv_cache_append.argtypes = [ctypes.c_void_p] * 8 + [ctypes.POINTER(DecodeShape), ctypes.c_void_p]
         L.chunked_prefill_attention.argtypes = [ctypes.c_void_p] * 6 + [ctypes.c_float] + [ctypes.c_void_p] * 3 + [
             ctypes.POINTER(PrefillShape), ctypes.c_void_p]
@@ -316,6 +319,17 @@ def paged_decode_attention(q, k_blocks, v_blocks, block_tables, context_lens, sc
         q.data_ptr(), k_blocks.data_ptr(), v_blocks.data_ptr(), block_tables.data_ptr(), context_lens.data_ptr(),
         float(scale), k_scale.data_ptr() if k_scale is not None else None,
         v_scale.data_ptr() if v_scale is not None else None, out.data_ptr(), ctypes.byref(shape), ws_ptr, ws_bytes,
+        _stream_ptr(stream)))
+
+
+def paged_decode_attention_noalloc(q, k_blocks, v_blocks, block_tables, context_lens, scale, out,
+                                   shape: DecodeShape, k_scale=None, v_scale=None, stream=None) -> None:
+    """Enqueue the decode without a workspace (the library's fixed per-GPU scratch;
+    include/dpool.h, paged_decode_attention_noalloc)."""
+    check(lib().paged_decode_attention_noalloc(
+        q.data_ptr(), k_blocks.data_ptr(), v_blocks.data_ptr(), block_tables.data_ptr(), context_lens.data_ptr(),
+        float(scale), k_scale.data_ptr() if k_scale is not None else None,
+        v_scale.data_ptr() if v_scale is not None else None, out.data_ptr(), ctypes.byref(shape),
         _stream_ptr(stream)))
 
 

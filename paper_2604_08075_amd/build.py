@@ -23,7 +23,7 @@ LIB = os.path.join(PKG, "libdpool.so")
 ARCH = "gfx950"
 
 HOST_SOURCES = ["status.cpp", "kv_pool.cpp", "route.cpp", "cost.cpp"]
-HIP_SOURCES = ["paged_decode.hip", "kv_append.hip", "prefill.hip", "hbm_probe.hip"]
+HIP_SOURCES = ["paged_decode.hip", "paged_decode_noalloc.hip", "kv_append.hip", "prefill.hip", "hbm_probe.hip"]
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
              "-Wall", "-Wno-unused-function"]
