@@ -14,7 +14,9 @@ from dataclasses import dataclass
 import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libdpool.so")
+# DPOOL_LIB selects another build of the same library (the host-sanitizer
+# build of build_sanitize.py, for the CPU tests)
+LIB_PATH = os.environ.get("DPOOL_LIB") or os.path.join(_PKG, "libdpool.so")
 
 DP_OK = 0
 DP_EIO = -5
