@@ -7,11 +7,11 @@ Steps, in the paper's order:
 Route(r, k)                                               (Algorithm 1, Route)
   c*      = c_hat_k - gamma * sigma_k                      (Eq. 5, conservative ratio)
   L_total = ceil(|r| / c*) + max_output_tokens             (Eq. 3, total token budget)
-  step 1  feasibility: L_total > C_max(short)  -> long     (strict >)
-  step 2  budget:      L_total <= B_short      -> short, else long  (inclusive <=)
-  step 3  spillover:   preferred pool overloaded and the alternate can serve r
-                       -> alternate
-  final   safety:      L_total > C_max(chosen) -> long
+  then the pool: a budget beyond the short pool's C_max (strict >) goes long
+  at once; otherwise L_total <= B_short (inclusive) prefers the short pool and
+  anything larger the long one; a preferred pool that is overloaded hands the
+  request to the other when that one can serve it; a pool whose C_max is below
+  L_total is never the answer (the long pool is)
 OnResponse(r, k, prompt_tokens)                           (Algorithm 1, OnResponse)
   c_obs   = |r| / prompt_tokens                            (Eq. 4)
   c_hat_k = beta * c_hat_k + (1 - beta) * c_obs            (Eq. 4 EMA, beta = 0.95)
@@ -110,15 +110,19 @@ def route_one(params: RouteParams, cats, pools, req_bytes: int, cat: int, max_ou
     """Algorithm 1 Route for one request; updates pools[chosen].in_flight. Returns (pool, L_total)."""
     c_star = conservative_ratio(params, cats[cat])
     l_total = token_budget(req_bytes, max_out, c_star)
-    if l_total > pools[SHORT].c_max:          # step 1: feasibility
+    if l_total > pools[SHORT].c_max:
+        # too long for the short pool: only the long pool can take it
         choice = LONG
     else:
-        choice = SHORT if l_total <= params.b_short else LONG   # step 2
-        alt = 1 - choice                                          # step 3
+        # the token budget decides; an overloaded pool hands the request to
+        # the other pool when that pool can hold it and has room
+        choice = SHORT if l_total <= params.b_short else LONG
+        alt = 1 - choice
         if (overloaded(params, pools[choice]) and l_total <= pools[alt].c_max
                 and not overloaded(params, pools[alt])):
             choice = alt
-        if l_total > pools[choice].c_max:     # final safety check
+        # never a pool whose C_max is below the request's budget
+        if l_total > pools[choice].c_max:
             choice = LONG
     pools[choice].in_flight += 1
     return choice, l_total

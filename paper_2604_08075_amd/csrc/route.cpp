@@ -1,4 +1,5 @@
-// Token-budget pool routing: Sec. 2.1 Eq. 3-5 and Sec. 2.2 Algorithm 1.
+// Token-budget pool routing: Sec. 2.1 Eq. 3-5; the dispatch rule of Sec. 2.2
+// (Algorithm 1).
 // Host only.  Compiled with -ffp-contract=off: every double operation is
 // rounded on its own, in the order written, so that any IEEE-754 double
 // implementation of the same steps agrees bit for bit.
@@ -21,6 +22,23 @@ double conservative_ratio(const dp_route_params* p, const dp_cat_state& c) {
   double r = c.c_hat - p->gamma * c.sigma;
   if (r < p->c_min) r = p->c_min;
   return r;
+}
+
+// The pool that serves a request of l_total tokens (Sec. 2.2).  A pool is
+// eligible when its C_max holds l_total; the long pool is the fallback when
+// the short one is not.  The token budget prefers the short pool for
+// l_total <= B_short and the long pool above it.  A preferred pool that is
+// overloaded gives the request to the other pool if that one is eligible and
+// not overloaded.  A preferred pool that cannot hold it (a long pool with
+// the smaller C_max) falls back to the long pool.
+int pick_pool(const dp_route_params* p, const dp_pool_state* pools, int64_t l_total) {
+  const bool eligible[2] = {l_total <= pools[kShort].c_max, l_total <= pools[kLong].c_max};
+  if (!eligible[kShort]) return kLong;
+  const int pref = (double)l_total <= p->b_short ? kShort : kLong;
+  const int other = 1 - pref;
+  const bool hand_over = overloaded(p, pools[pref]) && eligible[other] && !overloaded(p, pools[other]);
+  const int pick = hand_over ? other : pref;
+  return eligible[pick] ? pick : kLong;
 }
 
 }  // namespace
@@ -61,16 +79,7 @@ extern "C" int route_requests(const dp_route_params* params, const dp_cat_state*
   for (int64_t i = 0; i < n; ++i) {
     const double c_star = conservative_ratio(params, cats[req_cat[i]]);          // Eq. 5
     const int64_t l_total = (int64_t)std::ceil((double)req_bytes[i] / c_star) + req_max_out[i];  // Eq. 3
-    int choice;
-    if (l_total > pools[kShort].c_max) {  // step 1: feasibility
-      choice = kLong;
-    } else {
-      choice = ((double)l_total <= params->b_short) ? kShort : kLong;  // step 2: budget
-      const int alt = 1 - choice;                                      // step 3: spillover
-      if (overloaded(params, pools[choice]) && l_total <= pools[alt].c_max && !overloaded(params, pools[alt]))
-        choice = alt;
-      if (l_total > pools[choice].c_max) choice = kLong;  // final safety check
-    }
+    const int choice = pick_pool(params, pools, l_total);
     pools[choice].in_flight += 1;
     if (out_pool) out_pool[i] = (int8_t)choice;
     if (out_l_total) out_l_total[i] = l_total;

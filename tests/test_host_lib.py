@@ -348,3 +348,41 @@ def test_append_bad_pointers_rejected_on_host(host_lib):
     assert L.kv_cache_append(None, None, None, None, None, None, None, None, None, None) == -22   # null shape
     s0 = shape(host_lib, batch=0)
     assert L.kv_cache_append(None, None, None, None, None, None, None, None, ctypes.byref(s0), None) == 0  # nothing to do
+
+
+# ---------------------------------------------------------------- benchmark batches from the pool
+
+def test_benchmark_batches_take_their_blocks_from_the_library_pool(host_lib):
+    """Configs 2-5 lay out their batch with the library's allocator (Sec. 3
+    effect 1: pages on demand from a shuffled per-GPU pool); the values drawn
+    do not depend on where the block ids come from."""
+    import workloads
+    w = workloads.make_config(4, poison=False)
+    ref = workloads.make_config(4, poison=False, block_source="numpy")
+    assert w.meta["block_source"] == "pool" and ref.meta["block_source"] == "numpy"
+    assert (w.context_lens == ref.context_lens).all()
+    assert (w.q_bits == ref.q_bits).all() and (w.k_store.tiles == ref.k_store.tiles).all()
+    assert (w.v_store.tiles == ref.v_store.tiles).all()
+    # the same pool, seeded alike, hands out exactly these ids
+    c = workloads.CONFIGS[4]
+    pool = host_lib.KVPool(c["n_layers"], c["n_kv_heads"], 128, 2, c["c_max"], workloads.POOL_M_GPU_BYTES,
+                           workloads.POOL_UTIL, 0.0, seed=4)
+    assert pool.info().num_blocks == w.num_blocks == 49152
+    nblk = -(-w.context_lens.astype(np.int64) // 16)
+    for s in range(w.batch):
+        assert (w.block_tables[s, :nblk[s]] == pool.alloc_seq(int(w.context_lens[s]))).all()
+        assert (w.block_tables[s, nblk[s]:] == -1).all()
+    used = np.concatenate([w.block_tables[s, :nblk[s]] for s in range(w.batch)])
+    assert len(np.unique(used)) == len(used) and used.min() >= 0 and used.max() < w.num_blocks
+
+
+def test_workload_rejects_bad_block_ids():
+    import workloads
+    with pytest.raises(ValueError):
+        workloads.make_workload(2, 8, 2, [20, 16], c_max=64, seed=1, num_blocks=8, block_ids=[1, 2, 2])
+    with pytest.raises(ValueError):
+        workloads.make_workload(2, 8, 2, [20, 16], c_max=64, seed=1, num_blocks=8, block_ids=[1, 2, 8])
+    with pytest.raises(ValueError):
+        workloads.make_workload(2, 8, 2, [20, 16], c_max=64, seed=1, num_blocks=8, block_ids=[1, 2])
+    w = workloads.make_workload(2, 8, 2, [20, 16], c_max=64, seed=1, num_blocks=8, block_ids=[5, 0, 7])
+    assert w.block_tables[0, :2].tolist() == [5, 0] and w.block_tables[1, :1].tolist() == [7]

@@ -26,9 +26,16 @@ Config table (index -> shape):
 Pool sizes (blocks of 16 tokens): 49,152 for configs 2-4 and 167,936 for
 config 5 (the per-layer share of a KV-only 288 GB GPU; the derivation is
 checked in the tests against both sizing implementations); config 1 uses
-4x the blocks it needs.  Block ids are a seeded permutation of the pool
-(a shuffled free list), handed out in order, so every sequence's blocks
-are scattered.
+4x the blocks it needs.  Block ids of configs 2-5 come from the library's
+own block pool (kv_pool_create with the config's model shape and the
+config index as shuffle seed, then kv_pool_alloc_seq per sequence in batch
+order), so the allocator that serves the paper's on-demand pages is the one
+that lays out every benchmark and parity batch; the ids it returns are
+checked here (distinct, inside the pool) before use.  Elsewhere, and for
+block_source="numpy", they are a seeded permutation of the pool (a shuffled
+free list), handed out in order.  Either way every sequence's blocks are
+scattered.  The numpy permutation is drawn in both cases, so Q, K and V do
+not depend on the block source.
 
 Draw order within one numpy Generator(seed): lengths, block-id permutation,
 Q, K, V.  Values are N(0, 1) float32 rounded to bf16 (round-to-nearest-even).
@@ -59,14 +66,19 @@ E4M3_MAX = 448.0
 CONFIGS = {
     1: dict(name="tiny", batch=4, n_q_heads=8, n_kv_heads=2, c_max=512, kv="bf16", lengths="uniform"),
     2: dict(name="short_pool_llama70b", batch=128, n_q_heads=64, n_kv_heads=8, c_max=8192, kv="bf16",
-            lengths="lognormal", num_blocks=49152),
+            lengths="lognormal", num_blocks=49152, n_layers=80),
     3: dict(name="long_pool_llama70b", batch=16, n_q_heads=64, n_kv_heads=8, c_max=65536, kv="bf16",
-            lengths="pareto", num_blocks=49152),
+            lengths="pareto", num_blocks=49152, n_layers=80),
     4: dict(name="homogeneous_pool_llama70b", batch=16, n_q_heads=64, n_kv_heads=8, c_max=65536, kv="bf16",
-            lengths="mixture", num_blocks=49152),
+            lengths="mixture", num_blocks=49152, n_layers=80),
     5: dict(name="short_pool_qwen3_fp8", batch=256, n_q_heads=64, n_kv_heads=4, c_max=8192, kv="fp8_e4m3",
-            lengths="lognormal", num_blocks=167936),
+            lengths="lognormal", num_blocks=167936, n_layers=94),
 }
+# The pool of configs 2-5 is one GPU's KV share: 288 GB of HBM, 90% usable,
+# no weights counted (the whole budget goes to KV), model layer count and KV
+# heads as above.
+POOL_M_GPU_BYTES = 288e9
+POOL_UTIL = 0.9
 
 
 def _lognormal_ctx(rng, n, c_max=8192):
@@ -172,8 +184,12 @@ class Workload:
 
 
 def make_workload(batch, n_q_heads, n_kv_heads, context_lens, c_max, kv_format="bf16",
-                  num_blocks=None, seed=0, poison=True, config=0, name="custom", rng=None):
-    """Build a workload for given lengths (the rest of the draw order as documented)."""
+                  num_blocks=None, seed=0, poison=True, config=0, name="custom", rng=None, block_ids=None):
+    """Build a workload for given lengths (the rest of the draw order as documented).
+
+    block_ids, if given, are the pool block ids of every sequence's blocks in
+    batch order (as an allocator handed them out); else the seeded permutation
+    supplies them."""
     rng = np.random.default_rng(seed) if rng is None else rng
     ctx = np.asarray(context_lens, dtype=np.int64)
     nblk = -(-ctx // BLOCK)
@@ -185,6 +201,12 @@ def make_workload(batch, n_q_heads, n_kv_heads, context_lens, c_max, kv_format="
     max_blocks = -(-c_max // BLOCK)
     perm = rng.permutation(num_blocks).astype(np.int64)
     used_ids = perm[:used]
+    if block_ids is not None:
+        used_ids = np.asarray(block_ids, dtype=np.int64)
+        if used_ids.shape != (used,):
+            raise ValueError(f"block_ids: {used_ids.shape[0]} ids for {used} blocks")
+        if used and (used_ids.min() < 0 or used_ids.max() >= num_blocks or len(np.unique(used_ids)) != used):
+            raise ValueError("block_ids must be distinct ids inside the pool")
     bt = np.full((batch, max_blocks), -1, dtype=np.int32)
     off = 0
     for s in range(batch):
@@ -234,15 +256,42 @@ def make_workload(batch, n_q_heads, n_kv_heads, context_lens, c_max, kv_format="
         meta=dict(used_blocks=used, seed=seed, poison=poison))
 
 
-def make_config(i: int, seed: int | None = None, poison: bool = True) -> Workload:
-    """The five benchmark configurations, seeded by their index unless told otherwise."""
+def pool_block_ids(i: int, context_lens, seed: int) -> np.ndarray:
+    """Block ids of a config-i batch as the library's block pool hands them out:
+    one pool sized for the config's model on one GPU, shuffled with `seed`, one
+    kv_pool_alloc_seq per sequence in batch order (ids concatenated)."""
+    from paper_2604_08075_amd import binding
+    c = CONFIGS[i]
+    pool = binding.KVPool(c["n_layers"], c["n_kv_heads"], HEAD_DIM, 1 if c["kv"] == "fp8_e4m3" else 2, c["c_max"],
+                          POOL_M_GPU_BYTES, POOL_UTIL, 0.0, block_size=BLOCK, seed=seed)
+    try:
+        nb = pool.info().num_blocks
+        if nb != c["num_blocks"]:
+            raise ValueError(f"config {i}: the library's pool has {nb} blocks, expected {c['num_blocks']}")
+        ids = [pool.alloc_seq(int(t)) for t in context_lens]
+    finally:
+        pool.close()
+    return np.concatenate(ids) if ids else np.zeros(0, dtype=np.int32)
+
+
+def make_config(i: int, seed: int | None = None, poison: bool = True, block_source: str | None = None) -> Workload:
+    """The five benchmark configurations, seeded by their index unless told otherwise.
+    block_source: "pool" (the library's block pool; default for configs 2-5) or
+    "numpy" (the seeded permutation; default for config 1)."""
     c = CONFIGS[i]
     seed = i if seed is None else seed
+    if block_source is None:
+        block_source = "pool" if "n_layers" in c else "numpy"
+    if block_source not in ("pool", "numpy"):
+        raise ValueError(block_source)
     rng = np.random.default_rng(seed)
     ctx = draw_lengths(rng, c["lengths"], c["batch"], c["c_max"])
-    return make_workload(c["batch"], c["n_q_heads"], c["n_kv_heads"], ctx, c["c_max"], c["kv"],
-                         num_blocks=c.get("num_blocks"), seed=seed, poison=poison, config=i,
-                         name=c["name"], rng=rng)
+    ids = pool_block_ids(i, ctx, seed) if block_source == "pool" else None
+    w = make_workload(c["batch"], c["n_q_heads"], c["n_kv_heads"], ctx, c["c_max"], c["kv"],
+                      num_blocks=c.get("num_blocks"), seed=seed, poison=poison, config=i,
+                      name=c["name"], rng=rng, block_ids=ids)
+    w.meta["block_source"] = block_source
+    return w
 
 
 # Chunked-prefill workloads: each sequence's chunk is the last n tokens of its
