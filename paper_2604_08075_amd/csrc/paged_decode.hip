@@ -52,6 +52,7 @@
 #include <cmath>
 #include <cstdint>
 #include <mutex>
+#include <type_traits>
 
 #include "common.h"
 
@@ -205,22 +206,29 @@ __device__ __forceinline__ void store_out8(const DecodeArgs& a, size_t off, f32x
 // 2 * waves + k holds the merged record of the group of pieces whose last
 // piece is wave k's.  A record is (o, m, l): o normalised by l, m in log2
 // units.  Pieces are merged in groups of kFanIn consecutive pieces, then the
-// group records, so that no merge folds more than kFanIn records per memory
-// round trip on each level (a long segment can be cut into many pieces).
+// group records, so that a long segment cut into many pieces needs few
+// memory round trips on each level.
 constexpr int kFanIn = 8;
-
 
 // Log-sum-exp fold of records, by one wave, in record order:
 // M = max_p m_p, w_p = l_p 2^(m_p - M), o = sum_p w_p o_p / sum_p w_p,
-// L = sum_p w_p.  Each lane folds two (head, 8-value chunk) pairs at a time.
+// L = sum_p w_p.  Each lane folds NP (head, 8-value chunk) pairs: NP = 2
+// covers the 128 pairs of a GQA group of up to 8 heads, NP = 4 the 256 pairs
+// of up to 16, so one pass over the records covers every pair of the group.
+template <int NP>
 struct Fold {
-  float M[2], L[2];
-  f32x4 o0[2], o1[2];
+  float M[NP], L[NP];
+  f32x4 o0[NP], o1[NP];
 };
 
-__device__ __forceinline__ void fold_init(Fold& F) {
+// Records fetched per memory round trip: the same registers for either NP.
+template <int NP>
+constexpr int kRound = 16 / NP;
+
+template <int NP>
+__device__ __forceinline__ void fold_init(Fold<NP>& F) {
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < NP; ++i) {
     F.M[i] = -INFINITY;
     F.L[i] = 0.f;
     F.o0[i] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -228,159 +236,127 @@ __device__ __forceinline__ void fold_init(Fold& F) {
   }
 }
 
-// Fold records 0 .. n-1 in order.  rec(u, m, l, x0, x1) fetches record u's
-// values for both pairs; the fetches of kFanIn records are issued before
-// any of them is folded (one memory round trip per kFanIn records).
-template <class Rec>
-__device__ __forceinline__ void fold_records(Fold& F, int n, Rec rec) {
-  for (int r0 = 0; r0 < n; r0 += kFanIn) {
-    float m[kFanIn][2], l[kFanIn][2];
-    f32x4 x0[kFanIn][2], x1[kFanIn][2];
+template <int NP>
+__device__ __forceinline__ void fold_one(Fold<NP>& F, const float (&m)[NP], const float (&l)[NP],
+                                         const f32x4 (&x0)[NP], const f32x4 (&x1)[NP]) {
 #pragma unroll
-    for (int u = 0; u < kFanIn; ++u)
-      if (r0 + u < n) rec(r0 + u, m[u], l[u], x0[u], x1[u]);
-#pragma unroll
-    for (int u = 0; u < kFanIn; ++u) {
-      if (r0 + u < n) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          const float M2 = fmaxf(F.M[i], m[u][i]);
-          const float c_old = __builtin_amdgcn_exp2f(F.M[i] - M2);
-          const float c_new = l[u][i] * __builtin_amdgcn_exp2f(m[u][i] - M2);
-          F.o0[i] = F.o0[i] * c_old + x0[u][i] * c_new;
-          F.o1[i] = F.o1[i] * c_old + x1[u][i] * c_new;
-          F.L[i] = F.L[i] * c_old + c_new;
-          F.M[i] = M2;
-        }
-      }
-    }
+  for (int i = 0; i < NP; ++i) {
+    const float M2 = fmaxf(F.M[i], m[i]);
+    const float c_old = __builtin_amdgcn_exp2f(F.M[i] - M2);
+    const float c_new = l[i] * __builtin_amdgcn_exp2f(m[i] - M2);
+    F.o0[i] = F.o0[i] * c_old + x0[i] * c_new;
+    F.o1[i] = F.o1[i] * c_old + x1[i] * c_new;
+    F.L[i] = F.L[i] * c_old + c_new;
+    F.M[i] = M2;
   }
 }
 
-// The (head, first dim) of this lane's pairs in pass p0 (idle lanes re-read pair 0).
-__device__ __forceinline__ void pair_of(int p0, int lane, int npairs, int (&hd)[2], int (&d0)[2], bool (&ok)[2]) {
+// Fold records 0 .. n-1 in order.  rec(u, m, l, x0, x1) fetches record u's
+// values for every pair of the lane; the fetches of kRound records are
+// issued before any of them is folded.
+template <int NP, class Rec>
+__device__ __forceinline__ void fold_records(Fold<NP>& F, int n, Rec rec) {
+  constexpr int R = kRound<NP>;
+  for (int r0 = 0; r0 < n; r0 += R) {
+    float m[R][NP], l[R][NP];
+    f32x4 x0[R][NP], x1[R][NP];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int p = p0 + lane + 64 * i;
-    ok[i] = p < npairs;
-    const int pp = ok[i] ? p : 0;
-    hd[i] = pp >> 4;
-    d0[i] = (pp & 15) * 8;
+    for (int u = 0; u < R; ++u)
+      if (r0 + u < n) rec(r0 + u, m[u], l[u], x0[u], x1[u]);
+#pragma unroll
+    for (int u = 0; u < R; ++u)
+      if (r0 + u < n) fold_one<NP>(F, m[u], l[u], x0[u], x1[u]);
   }
+}
+
+// The (head, first dim) of each pair of this lane (idle lanes re-read pair 0).
+template <int NP>
+struct Pairs {
+  int hd[NP], d0[NP];
+  bool ok[NP];
+};
+
+template <int NP>
+__device__ __forceinline__ Pairs<NP> pairs_of(int lane, int npairs) {
+  Pairs<NP> P;
+#pragma unroll
+  for (int i = 0; i < NP; ++i) {
+    const int p = lane + 64 * i;
+    P.ok[i] = p < npairs;
+    const int pp = P.ok[i] ? p : 0;
+    P.hd[i] = pp >> 4;
+    P.d0[i] = (pp & 15) * 8;
+  }
+  return P;
 }
 
 // Record u from global slot `slot`, or (own) from this wave's LDS staging
 // entry `own`: eight [lane] chunks of 4 floats (dims 16 nn + 4 lj .. + 4 of
 // head li at lane li + 16 lj), then each lane's (m, l).
-__device__ __forceinline__ void fetch_record(const DecodeArgs& a, size_t slot, const char* own, const int (&hd)[2],
-                                             const int (&d0)[2], float (&m)[2], float (&l)[2], f32x4 (&x0)[2],
-                                             f32x4 (&x1)[2]) {
+template <int NP>
+__device__ __forceinline__ void fetch_record(const DecodeArgs& a, size_t slot, const char* own, const Pairs<NP>& P,
+                                             float (&m)[NP], float (&l)[NP], f32x4 (&x0)[NP], f32x4 (&x1)[NP]) {
   const int G = a.group;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < NP; ++i) {
+    const int hd = P.hd[i], d0 = P.d0[i];
     if (own) {
-      const float* ml = (const float*)(own + 8192 + hd[i] * 8);
+      const float* ml = (const float*)(own + 8192 + hd * 8);
       m[i] = ml[0];
       l[i] = ml[1];
-      const int nn = d0[i] >> 4, q = (d0[i] & 15) >> 2;
-      x0[i] = *(const f32x4*)(own + nn * 1024 + (hd[i] + 16 * q) * 16);
-      x1[i] = *(const f32x4*)(own + nn * 1024 + (hd[i] + 16 * (q + 1)) * 16);
+      const int nn = d0 >> 4, q = (d0 & 15) >> 2;
+      x0[i] = *(const f32x4*)(own + nn * 1024 + (hd + 16 * q) * 16);
+      x1[i] = *(const f32x4*)(own + nn * 1024 + (hd + 16 * (q + 1)) * 16);
     } else {
-      coherent_load2(a.rec_ml + (slot * G + hd[i]) * 2, m[i], l[i]);
-      const float* ro = a.rec_o + (slot * G + hd[i]) * kHeadDim + d0[i];
+      coherent_load2(a.rec_ml + (slot * G + hd) * 2, m[i], l[i]);
+      const float* ro = a.rec_o + (slot * G + hd) * kHeadDim + d0;
       x0[i] = coherent_load4(ro);
       x1[i] = coherent_load4(ro + 4);
     }
   }
 }
 
-// Merge n records (slot_of(i) names the i-th; record own_idx, if >= 0, is
-// this wave's LDS entry `own`) into the output rows of segment (s, g), or
-// into record slot dst.
-template <class SlotOf>
-__device__ __forceinline__ void merge_records(const DecodeArgs& a, SlotOf slot_of, int n, bool to_out, int s, int g,
-                                              size_t dst, int lane, int own_idx = -1, const char* own = nullptr) {
-  const int G = a.group;
-  const int npairs = G * 16;  // (head, 8-value chunk) pairs
-  for (int p0 = 0; p0 < npairs; p0 += 128) {  // two pairs per lane at a time
-    int hd[2], d0[2];
-    bool ok[2];
-    pair_of(p0, lane, npairs, hd, d0, ok);
-    Fold F;
-    fold_init(F);
-    fold_records(F, n, [&](int u, float(&m)[2], float(&l)[2], f32x4(&x0)[2], f32x4(&x1)[2])
-                           __attribute__((always_inline)) {
-                             fetch_record(a, u == own_idx ? 0 : slot_of(u), u == own_idx ? own : nullptr, hd, d0, m, l,
-                                          x0, x1);
-                           });
-    for (int i = 0; i < 2; ++i) {
-      if (!ok[i]) continue;
-      const float inv = 1.0f / F.L[i];
-      if (to_out) {
-        store_out8(a, ((size_t)s * a.hq + (size_t)g * G + hd[i]) * kHeadDim + d0[i], F.o0[i] * inv, F.o1[i] * inv);
-      } else {
-        float* ro = a.rec_o + (dst * G + hd[i]) * kHeadDim + d0[i];
-        coherent_store4(ro, F.o0[i] * inv);
-        coherent_store4(ro + 4, F.o1[i] * inv);
-        if (d0[i] == 0) coherent_store2(a.rec_ml + (dst * G + hd[i]) * 2, F.M[i], F.L[i]);
-      }
-    }
+// The fold normalised: exactly what a record of it holds (o / L, M, L).
+template <int NP>
+__device__ __forceinline__ void normalise(const Fold<NP>& F, float (&m)[NP], float (&l)[NP], f32x4 (&x0)[NP],
+                                          f32x4 (&x1)[NP]) {
+#pragma unroll
+  for (int i = 0; i < NP; ++i) {
+    const float inv = 1.0f / F.L[i];
+    x0[i] = F.o0[i] * inv;
+    x1[i] = F.o1[i] * inv;
+    m[i] = F.M[i];
+    l[i] = F.L[i];
   }
 }
 
-// Both merge levels at once, by the wave that completes the last group of a
-// segment: its group's members are folded (record own_idx from LDS) into the
-// values the group record would hold, and those take group c_own's place in
-// the fold of all groups into the output rows.  The result is bit-identical
-// to storing the group record and merging it from memory.
-template <class MemberOf, class GroupOf>
-__device__ __forceinline__ void merge_group_then_segment(const DecodeArgs& a, MemberOf member_of, int gn, int own_idx,
-                                                         const char* own, GroupOf group_of, int ngroups, int c_own,
-                                                         int s, int g, int lane) {
+// Write the fold as the output rows of segment (s, g).
+template <int NP>
+__device__ __forceinline__ void write_rows(const DecodeArgs& a, const Fold<NP>& F, const Pairs<NP>& P, int s,
+                                           int g) {
   const int G = a.group;
-  const int npairs = G * 16;
-  for (int p0 = 0; p0 < npairs; p0 += 128) {
-    int hd[2], d0[2];
-    bool ok[2];
-    pair_of(p0, lane, npairs, hd, d0, ok);
-    Fold Fg;
-    fold_init(Fg);
-    fold_records(Fg, gn, [&](int u, float(&m)[2], float(&l)[2], f32x4(&x0)[2], f32x4(&x1)[2])
-                             __attribute__((always_inline)) {
-                               fetch_record(a, u == own_idx ? 0 : member_of(u), u == own_idx ? own : nullptr, hd, d0, m,
-                                            l, x0, x1);
-                             });
-    float gm[2], gl[2];
-    f32x4 gx0[2], gx1[2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {  // exactly what the group record would hold
-      const float inv = 1.0f / Fg.L[i];
-      gx0[i] = Fg.o0[i] * inv;
-      gx1[i] = Fg.o1[i] * inv;
-      gm[i] = Fg.M[i];
-      gl[i] = Fg.L[i];
-    }
-    Fold F;
-    fold_init(F);
-    fold_records(F, ngroups, [&](int u, float(&m)[2], float(&l)[2], f32x4(&x0)[2], f32x4(&x1)[2])
-                                 __attribute__((always_inline)) {
-                                   if (u == c_own) {
+  for (int i = 0; i < NP; ++i) {
+    if (!P.ok[i]) continue;
+    const float inv = 1.0f / F.L[i];
+    store_out8(a, ((size_t)s * a.hq + (size_t)g * G + P.hd[i]) * kHeadDim + P.d0[i], F.o0[i] * inv,
+               F.o1[i] * inv);
+  }
+}
+
+// Write normalised values as record slot dst.
+template <int NP>
+__device__ __forceinline__ void write_record(const DecodeArgs& a, const Pairs<NP>& P, size_t dst,
+                                             const float (&m)[NP], const float (&l)[NP], const f32x4 (&x0)[NP],
+                                             const f32x4 (&x1)[NP]) {
+  const int G = a.group;
 #pragma unroll
-                                     for (int i = 0; i < 2; ++i) {
-                                       m[i] = gm[i];
-                                       l[i] = gl[i];
-                                       x0[i] = gx0[i];
-                                       x1[i] = gx1[i];
-                                     }
-                                   } else {
-                                     fetch_record(a, group_of(u), nullptr, hd, d0, m, l, x0, x1);
-                                   }
-                                 });
-    for (int i = 0; i < 2; ++i) {
-      if (!ok[i]) continue;
-      const float inv = 1.0f / F.L[i];
-      store_out8(a, ((size_t)s * a.hq + (size_t)g * G + hd[i]) * kHeadDim + d0[i], F.o0[i] * inv, F.o1[i] * inv);
-    }
+  for (int i = 0; i < NP; ++i) {
+    if (!P.ok[i]) continue;
+    float* ro = a.rec_o + (dst * G + P.hd[i]) * kHeadDim + P.d0[i];
+    coherent_store4(ro, x0[i]);
+    coherent_store4(ro + 4, x1[i]);
+    if (P.d0[i] == 0) coherent_store2(a.rec_ml + (dst * G + P.hd[i]) * 2, m[i], l[i]);
   }
 }
 
@@ -573,11 +549,17 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   // chunk-major ([nn][lane]), then for a record each lane's (m, l).
   char* const stg = stage_lds[w];
   int st_n = 0, st_off = 0;  // entries and bytes staged (wave-uniform)
-  auto flush = [&](int skip) __attribute__((always_inline)) {
+  int first_entry = -1;      // staging entry of the slice's first piece record while it is still staged
+  // pass 0 writes every entry and empties the staging area; pass 1 writes
+  // only the records (the entries in `skip`, a bit mask, excepted), pass 2
+  // only the rows, and empties it.
+  auto flush = [&](unsigned skip, int pass) __attribute__((always_inline)) {
+    if (pass == 0) first_entry = -1;  // the first piece's record is written out
     for (int e = 0; e < st_n; ++e) {
-      if (e == skip) continue;
+      if ((skip >> e) & 1u) continue;
       const int ko = __builtin_amdgcn_readfirstlane(stage_kind[w][e]);
       const int kind = ko & 15;
+      if ((pass == 1 && kind != 2) || (pass == 2 && kind == 2)) continue;
       const char* base = stg + (ko >> 4);
       const long long dst = stage_dst[w][e];
       const unsigned dlo = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)(dst & 0xffffffffll));
@@ -600,11 +582,13 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
         }
       }
     }
-    st_n = 0;
-    st_off = 0;
+    if (pass != 1) {
+      st_n = 0;
+      st_off = 0;
+    }
   };
   auto stage_begin = [&](int bytes) __attribute__((always_inline)) {  // room for one entry; returns its LDS offset
-    if (st_n == kMaxStaged || st_off + bytes > kStageBytes) flush(-1);
+    if (st_n == kMaxStaged || st_off + bytes > kStageBytes) flush(0u, 0);
     const int off = st_off;
     st_off += bytes;
     return off;
@@ -766,6 +750,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
         own_entry = st_n;
         own_x = piece_first ? 0 : 1;
       }
+      if (piece_first) first_entry = st_n;
       stage_meta(2, (int)(base - stg), (long long)gw * 2 + (piece_first ? 0 : 1));
       if (piece_first) {
         arr_s0 = cs.s;
@@ -856,46 +841,62 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     f.ngroups = (f.np + kFanIn - 1) / kFanIn;
     return f;
   };
-  // The piece ending the slice is usually the last of its group to arrive
-  // (the others finished earlier in their slices).  If the group counter
-  // already shows every other piece, this wave merges with its own partial
-  // straight from LDS: no record write, no wait for it, no increment.
-  bool own_last = false;
-  SegInfo own_f = {};
-  if (own_entry >= 0) {
-    own_f = seg_info(own_x == 0 ? arr_s0 : arr_s1, own_x == 0 ? arr_g0 : arr_g1);
-    int c = 0;
-    if (lane == 0) c = __hip_atomic_load(group_cnt(own_f.kg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    own_last = __shfl(c, 0) == own_f.gn - 1;
+  // Piece x = 0 is the slice's first split piece, x = 1 its last.  The
+  // staging entry of each, while its record is still in LDS:
+  const int ent0 = own_x == 0 ? own_entry : first_entry;
+  const int ent1 = own_x == 1 ? own_entry : -1;
+  SegInfo f0 = {}, f1 = {};
+  if (arr_s0 >= 0) f0 = seg_info(arr_s0, arr_g0);
+  if (arr_s1 >= 0) f1 = seg_info(arr_s1, arr_g1);
+  // If a group counter already shows every other piece of the group (read
+  // with an atomic load, far quicker than an increment's round trip), this
+  // wave is that group's last arrival: it merges with its own partial
+  // straight from LDS, with no record write, no wait for it and no
+  // increment.  Both counters are read together.
+  int c0 = 0, c1 = 0;
+  if (lane == 0) {
+    if (ent0 >= 0) c0 = __hip_atomic_load(group_cnt(f0.kg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (ent1 >= 0) c1 = __hip_atomic_load(group_cnt(f1.kg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  flush(own_last ? own_entry : -1);
-  if (arr_s0 >= 0 || arr_s1 >= 0) {
+  const bool mine0 = ent0 >= 0 && __shfl(c0, 0) == f0.gn - 1;
+  const bool mine1 = ent1 >= 0 && __shfl(c1, 0) == f1.gn - 1;
+  // Records first: they must have reached the coherence point before their
+  // arrivals are counted.  Finished rows go out after the counters, their
+  // stores overlapping the atomics' round trip.
+  flush((mine0 ? 1u << ent0 : 0u) | (mine1 ? 1u << ent1 : 0u), 1);
+  int old0 = 0, old1 = 0;
+  auto entry_ptr = [&](int e) __attribute__((always_inline)) {
+    return e >= 0 ? stg + (__builtin_amdgcn_readfirstlane(stage_kind[w][e]) >> 4) : nullptr;
+  };
+  const char* const rec0 = entry_ptr(ent0);
+  const char* const rec1 = entry_ptr(ent1);
+  if ((arr_s0 >= 0 && !mine0) || (arr_s1 >= 0 && !mine1)) {
     // this wave's record stores have completed (at the coherence point)
     // before it counts them
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    const char* own_rec = own_entry >= 0 ? stg + (__builtin_amdgcn_readfirstlane(stage_kind[w][own_entry]) >> 4) : nullptr;
     // Both pieces' arrivals are counted before either count is examined:
     // a device-wide atomic takes a few microseconds to return, and the two
     // would otherwise follow one another.
-    SegInfo f0 = {}, f1 = {};
-    int old0 = 0, old1 = 0;
-    if (arr_s0 >= 0) {
-      const bool mine = own_last && own_x == 0;
-      f0 = mine ? own_f : seg_info(arr_s0, arr_g0);
-      if (!mine && lane == 0)
-        old0 = __hip_atomic_fetch_add(group_cnt(f0.kg), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    if (arr_s1 >= 0) {
-      const bool mine = own_last && own_x == 1;
-      f1 = mine ? own_f : seg_info(arr_s1, arr_g1);
-      if (!mine && lane == 0)
-        old1 = __hip_atomic_fetch_add(group_cnt(f1.kg), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+    if (arr_s0 >= 0 && !mine0 && lane == 0)
+      old0 = __hip_atomic_fetch_add(group_cnt(f0.kg), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (arr_s1 >= 0 && !mine1 && lane == 0)
+      old1 = __hip_atomic_fetch_add(group_cnt(f1.kg), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  flush(0u, 2);
+  if (arr_s0 < 0 && arr_s1 < 0) return;
+
+  // The last arrival of a group merges it.  One pass over the records covers
+  // every (head, 8-value chunk) pair of the GQA group: two pairs per lane up
+  // to 8 heads, four up to 16.
+  auto merge_pieces = [&](auto np_c) __attribute__((always_inline)) {
+    constexpr int NP = decltype(np_c)::value;
+    const Pairs<NP> P = pairs_of<NP>(lane, G * 16);
     for (int x = 0; x < 2; ++x) {
       const int s = x == 0 ? arr_s0 : arr_s1;
       if (s < 0) continue;
       const int g = x == 0 ? arr_g0 : arr_g1;
-      const bool mine = own_last && x == own_x;
+      const bool mine = x == 0 ? mine0 : mine1;
+      const char* const own_rec = x == 0 ? rec0 : rec1;
       const SegInfo f = x == 0 ? f0 : f1;
       auto piece_slot = [&](int r) __attribute__((always_inline)) {
         return r == 0 ? (size_t)f.first_slot : (size_t)2 * (f.k0 + r);
@@ -903,37 +904,76 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       if (!mine && __shfl(x == 0 ? old0 : old1, 0) != f.gn - 1) continue;  // not the group's last arrival
       asm volatile("" ::: "memory");  // record loads are issued after this branch resolves
       if (lane == 0) __hip_atomic_store(group_cnt(f.kg), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (f.ngroups == 1) {
-        merge_records(a, piece_slot, f.np, true, s, g, 0, lane, mine ? f.r : -1, own_rec);
+      // the group's pieces, in order (this wave's own piece from LDS)
+      const int own_idx = mine ? f.r - f.gfirst : -1;
+      Fold<NP> Fg;
+      fold_init(Fg);
+      fold_records(Fg, f.gn, [&](int u, float(&m)[NP], float(&l)[NP], f32x4(&x0)[NP], f32x4(&x1)[NP])
+                                 __attribute__((always_inline)) {
+                                   fetch_record(a, u == own_idx ? 0 : piece_slot(f.gfirst + u),
+                                                u == own_idx ? own_rec : nullptr, P, m, l, x0, x1);
+                                 });
+      if (f.ngroups == 1) {  // the group is the whole segment
+        write_rows(a, Fg, P, s, g);
         continue;
       }
-      auto member_slot = [&](int i) __attribute__((always_inline)) { return piece_slot(f.gfirst + i); };
+      // Two levels.  This group's record, as it would be stored:
+      float gm[NP], gl[NP];
+      f32x4 gx0[NP], gx1[NP];
+      normalise(Fg, gm, gl, gx0, gx1);
       auto group_slot = [&](int c) __attribute__((always_inline)) {
         return (size_t)2 * TW + f.k0 + min(f.np, (c + 1) * kFanIn) - 1;
       };
-      // If every other group of the segment is already merged, merge this
-      // group and the segment in one pass: no group record, no wait for its
-      // store, no second counter round trip.
+      // If every other group of the segment is merged by now (checked after
+      // this group's fold, so that the others had that long to finish),
+      // finish the segment from here: no group record, no wait for its
+      // store, no second counter round trip.  Bit-identical to the path
+      // through memory.
       int done = 0;
       if (lane == 0) done = __hip_atomic_load(seg_cnt(f.kend), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int c_own = f.gfirst / kFanIn;
       if (__shfl(done, 0) == f.ngroups - 1) {
         asm volatile("" ::: "memory");  // group record loads are issued after this branch resolves
         if (lane == 0) __hip_atomic_store(seg_cnt(f.kend), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        merge_group_then_segment(a, member_slot, f.gn, mine ? f.r - f.gfirst : -1, own_rec, group_slot, f.ngroups,
-                                 f.gfirst / kFanIn, s, g, lane);
+        Fold<NP> F;
+        fold_init(F);
+        fold_records(F, f.ngroups, [&](int u, float(&m)[NP], float(&l)[NP], f32x4(&x0)[NP], f32x4(&x1)[NP])
+                                       __attribute__((always_inline)) {
+                                         if (u == c_own) {
+#pragma unroll
+                                           for (int i = 0; i < NP; ++i) {
+                                             m[i] = gm[i];
+                                             l[i] = gl[i];
+                                             x0[i] = gx0[i];
+                                             x1[i] = gx1[i];
+                                           }
+                                         } else {
+                                           fetch_record(a, group_slot(u), nullptr, P, m, l, x0, x1);
+                                         }
+                                       });
+        write_rows(a, F, P, s, g);
         continue;
       }
-      merge_records(a, member_slot, f.gn, false, s, g, (size_t)2 * TW + f.kg, lane, mine ? f.r - f.gfirst : -1,
-                    own_rec);
+      write_record(a, P, (size_t)2 * TW + f.kg, gm, gl, gx0, gx1);
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       int old = 0;
       if (lane == 0) old = __hip_atomic_fetch_add(seg_cnt(f.kend), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (__shfl(old, 0) != f.ngroups - 1) continue;
       asm volatile("" ::: "memory");
       if (lane == 0) __hip_atomic_store(seg_cnt(f.kend), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      merge_records(a, group_slot, f.ngroups, true, s, g, 0, lane);
+      Fold<NP> F;
+      fold_init(F);
+      fold_records(F, f.ngroups, [&](int u, float(&m)[NP], float(&l)[NP], f32x4(&x0)[NP], f32x4(&x1)[NP])
+                                     __attribute__((always_inline)) {
+                                       fetch_record(a, group_slot(u), nullptr, P, m, l, x0, x1);
+                                     });
+      write_rows(a, F, P, s, g);
     }
-  }
+  };
+  if (G > 8)
+    merge_pieces(std::integral_constant<int, 4>{});
+  else
+    merge_pieces(std::integral_constant<int, 2>{});
 }
 
 template __global__ void paged_decode_kernel<false>(DecodeArgs);
