@@ -16,7 +16,11 @@ its host launcher do it, and checks on random batches that
     kernel's tile list;
   * every piece of a cut segment writes the record slot its merger reads, the
     arrival counters and record slots stay inside the workspace, and no two
-    (segment, group) pairs share a counter.
+    (segment, group) pairs share a counter;
+  * the end-of-slice protocol (counters read first, records published before
+    they are counted, the last arrival merging) writes every cut segment once,
+    never reads an unpublished record and leaves every counter at zero, under
+    any interleaving of the waves' steps.
 
 A kernel change to any of these must be mirrored here.
 """
@@ -240,3 +244,119 @@ def test_benchmark_shapes():
             ctx = np.maximum(ctx, rng.integers(8192, 42000, B))
         sim = simulate(ctx, hkv, fp8, int(ctx.max()), cmax // 16)
         check(sim, hkv)
+
+
+# ---------------------------------------------------------------- end-of-slice merge protocol
+
+def run_merge_protocol(sim, rng, p_staged=0.8):
+    """Play the kernel's end-of-slice protocol for every split piece, with the
+    waves' steps interleaved in a random order, and check that every cut
+    segment is written exactly once, that no merge reads a record before it
+    is published, and that every counter is zero afterwards.
+
+    Per wave, as the kernel orders it: read both group counters (atomic
+    loads) for pieces whose record is still staged in LDS; publish and count
+    the pieces that were not found to be the group's last; then, piece by
+    piece, the group's last arrival merges the group (resetting its counter)
+    and either writes the segment or goes through the segment counter (load,
+    then group record and increment unless every other group is done)."""
+    C, pre = sim["C"], sim["pre"]
+    hkv = sim["hkv"]
+    seg_of_piece = {}
+    waves = {}
+    for (s, g), got in sim["pieces"].items():
+        nus = pre[s + 1] - pre[s]
+        a0 = hkv * pre[s] + g * nus
+        k0, kend = a0 // C, (a0 + nus - 1) // C
+        np_ = kend - k0 + 1
+        for r in range(np_):
+            gfirst = r - r % FAN_IN
+            gn = min(np_, gfirst + FAN_IN) - gfirst
+            info = dict(seg=(s, g), r=r, gfirst=gfirst, gn=gn, kg=k0 + gfirst + gn - 1, ngroups=-(-np_ // FAN_IN),
+                        kend=kend, np=np_)
+            w = k0 + r
+            seg_of_piece[(w, r == 0)] = info
+            waves.setdefault(w, []).append(info)
+    group_cnt, seg_cnt = {}, {}
+    published, group_published, written = set(), set(), {}
+
+    def merge_group(info, own):
+        seg = info["seg"]
+        for u in range(info["gn"]):
+            r = info["gfirst"] + u
+            if not (own and r == info["r"]):
+                assert (seg, r) in published, f"merge of {seg} read piece {r} before it was published"
+        group_cnt[info["kg"]] = 0
+
+    def steps_of(w):
+        pieces = sorted(waves[w], key=lambda i: i["r"] != 0)  # the slice's first piece, then its last
+        staged = [bool(rng.random() < p_staged) for _ in pieces]
+        mine = [False] * len(pieces)
+        # 1. atomic loads of the group counters (records still in LDS)
+        for x, info in enumerate(pieces):
+            if staged[x]:
+                mine[x] = group_cnt.get(info["kg"], 0) == info["gn"] - 1
+        yield
+        # 2. publish and count the others
+        last = [False] * len(pieces)
+        for x, info in enumerate(pieces):
+            if not mine[x]:
+                published.add((info["seg"], info["r"]))
+                old = group_cnt.get(info["kg"], 0)
+                group_cnt[info["kg"]] = old + 1
+                last[x] = old == info["gn"] - 1
+                yield
+        # 3. merges
+        for x, info in enumerate(pieces):
+            if not (mine[x] or last[x]):
+                continue
+            merge_group(info, mine[x])
+            yield
+            seg = info["seg"]
+            if info["ngroups"] == 1:
+                written[seg] = written.get(seg, 0) + 1
+                continue
+            c_own = info["gfirst"] // FAN_IN
+            if seg_cnt.get(info["kend"], 0) == info["ngroups"] - 1:
+                for c in range(info["ngroups"]):
+                    if c != c_own:
+                        assert (seg, c) in group_published, f"{seg}: group {c} read before it was published"
+                seg_cnt[info["kend"]] = 0
+                written[seg] = written.get(seg, 0) + 1
+                continue
+            group_published.add((seg, c_own))
+            old = seg_cnt.get(info["kend"], 0)
+            seg_cnt[info["kend"]] = old + 1
+            yield
+            if old == info["ngroups"] - 1:
+                for c in range(info["ngroups"]):
+                    assert (seg, c) in group_published
+                seg_cnt[info["kend"]] = 0
+                written[seg] = written.get(seg, 0) + 1
+
+    live = {w: steps_of(w) for w in waves}
+    while live:
+        w = list(live)[int(rng.integers(0, len(live)))]
+        try:
+            next(live[w])
+        except StopIteration:
+            del live[w]
+    assert written == {seg: 1 for seg in sim["pieces"]}, "a cut segment was written other than once"
+    assert all(v == 0 for v in group_cnt.values()) and all(v == 0 for v in seg_cnt.values())
+
+
+@pytest.mark.parametrize("trial", range(30))
+def test_merge_protocol_any_arrival_order(trial):
+    """Random batches (including long segments cut into more than eight pieces,
+    which merge on two levels) under random interleavings of the waves' steps."""
+    rng = np.random.default_rng(7000 + trial)
+    fp8 = bool(trial % 2)
+    B = int(rng.choice([2, 5, 16, 40]))
+    hkv = int(rng.choice([1, 2, 4]))
+    max_ctx = int(rng.choice([300, 3000, 20000]))
+    ctx = draw(rng, B, max_ctx, 0.2)
+    cus = int(rng.choice([2, 8, 32]))
+    sim = simulate(ctx, hkv, fp8, max_ctx, -(-max_ctx // 16), 0, 0, cus)
+    sim["hkv"] = hkv
+    for rep in range(3):
+        run_merge_protocol(sim, np.random.default_rng(rep + 10 * trial), p_staged=float(rng.choice([0.0, 0.5, 1.0])))
