@@ -13,13 +13,16 @@ bf16 KV, C_max 8192); the long pool (B=16, C_max 65536), the homogeneous
 pool (B=16, mixed lengths, C_max 65536) and the Qwen3-shaped fp8 short pool
 are reported beside it in the same line, as the metric compares the pools.
 Each pool also times the KV-cache append of its batch (one new token per
-sequence).  The line also carries:
+sequence).  Besides GB/s the line gives sequences x steps per second for
+one layer and, as context, for the attention of every layer of the model
+(divided by its 80 or 94 layers).  The line also carries:
   roofline      the decode kernel against 8 TB/s: algorithmic KV bytes over
                 the average launch duration of the timed region (back-to-back
                 launches between two HIP events on the launch stream), beside
                 the kernel-trace average and the HBM traffic of the committed
                 rocprofv3 summaries when they were taken on the source as it
-                is, and beside the read ceiling measured here;
+                is, the median of the event-bracketed launch times, and beside
+                the read ceiling measured here;
   hbm_read_ceiling  a plain 4 GiB read of device memory (contiguous, and as
                 4 KiB tiles in random order), timed the same way;
   cpu_baseline  the fp64 oracle timed on this host over the same batch, on
@@ -165,12 +168,17 @@ def measure(cfg: int, steps: int, warmup: int, partition_tokens: int, wgs: int, 
         step(i)
         ev[i][1].record()
     torch.cuda.synchronize()
-    bracket_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / steps
+    bracketed = sorted(e[0].elapsed_time(e[1]) for e in ev)
+    bracket_ms = sum(bracketed) / steps
+    bracket_median_ms = bracketed[steps // 2] if steps % 2 else 0.5 * (bracketed[steps // 2 - 1] + bracketed[steps // 2])
     res = dict(
         workload=describe(w), name=w.name, batch=w.batch, kv_bytes=w.kv_bytes, kv_format=w.kv_format,
         ms_per_step=ms_step, gbs=w.kv_bytes / (ms_step * 1e-3) / 1e9,
         pct_of_peak_hbm=100.0 * w.kv_bytes / (ms_step * 1e-3) / 1e9 / PEAK_HBM_GBS,
         seq_steps_per_s=w.batch / (ms_step * 1e-3), event_bracketed_launch_ms=bracket_ms,
+        event_bracketed_median_ms=bracket_median_ms,
+        # context: every layer of the model runs this attention once per decode step
+        model_layers=workloads.CONFIGS.get(cfg, {}).get("n_layers"),
         partition_tokens=dec.partition_tokens, layers_rotated=layers, sum_ctx=int(w.context_lens.sum()),
         flops=4 * w.head_dim * w.n_q_heads * int(w.context_lens.sum()))
     prof = profiled_kernel_avg_us(w.name)
@@ -483,6 +491,7 @@ def main():
             "timing": "average launch duration of the timed region: back-to-back launches between two HIP "
                       "events on the launch stream (inter-launch gaps included)",
             "event_bracketed_launch_ms": head["event_bracketed_launch_ms"],
+            "event_bracketed_median_ms": head["event_bracketed_median_ms"],
             "rocprof_kernel_avg_us": head.get("rocprof_kernel_avg_us"),
             "rocprof_frac": (head["rocprof_gbs"] / PEAK_HBM_GBS) if "rocprof_gbs" in head else None,
             "rocprof_profile": f"profiles/paged_decode_{head['name']}.txt" if "rocprof_gbs" in head else None}
@@ -498,6 +507,8 @@ def main():
                    "partition_tokens": head["partition_tokens"], "layers_rotated": head["layers_rotated"]},
         "pct_of_peak_hbm": head["pct_of_peak_hbm"],
         "seq_steps_per_s": head["seq_steps_per_s"],
+        "seq_steps_per_s_attention_all_layers": (head["seq_steps_per_s"] / head["model_layers"]
+                                                 if head.get("model_layers") else None),
         "kv_append": head["kv_append"],
         "roofline": roof,
     }
