@@ -155,29 +155,33 @@ __device__ __forceinline__ int units_of(int ctx) {
 }
 
 // Partial records cross compute units on different XCDs, whose L2 caches are
-// not coherent with each other.  They are written and read with agent-scope
-// atomic accesses (sc1: written through to, and read from, the coherence
-// point), so no L2-wide writeback or invalidate is needed: those stall every
-// wave streaming through the same L2.
-__device__ __forceinline__ void coherent_store4(float* p, f32x4 v) {
-  typedef unsigned long long u64;
-  typedef float f32x2 __attribute__((ext_vector_type(2)));
-  __hip_atomic_store((u64*)p, __builtin_bit_cast(u64, f32x2{v[0], v[1]}), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  __hip_atomic_store((u64*)p + 1, __builtin_bit_cast(u64, f32x2{v[2], v[3]}), __ATOMIC_RELAXED,
-                     __HIP_MEMORY_SCOPE_AGENT);
+// not coherent with each other.  They are written and read with the cache
+// policy of an agent-scope atomic access (sc1: written through to, and read
+// from, the coherence point), so no L2-wide writeback or invalidate is needed:
+// those stall every wave streaming through the same L2.  (m, l) pairs use
+// 8-byte agent-scope atomics; the o values use 16-byte buffer accesses with
+// the sc1 bit, which halves the instructions of a merge's record reads and
+// keeps a round of eight records under the 63 loads a wave can have in flight.
+constexpr int kSc1 = 16;                  // buffer cache-policy bit: sc1 (device scope)
+constexpr int kBufferWord3 = 0x00020000;  // buffer resource word 3 for gfx9: 32-bit data format
+// Record slot `slot` (G * 128 floats) as a buffer resource; its base is the
+// same for the whole wave, and an access outside the slot reads zero and
+// writes nothing.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t record_rsrc(float* rec_o, size_t slot, int G) {
+  const int sl = __builtin_amdgcn_readfirstlane((int)slot);
+  return __builtin_amdgcn_make_buffer_rsrc(rec_o + (size_t)sl * G * kHeadDim, (short)0, G * kHeadDim * 4,
+                                           kBufferWord3);
+}
+__device__ __forceinline__ void coherent_store16(__amdgpu_buffer_rsrc_t r, int byte_off, f32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, byte_off, 0, kSc1);
+}
+__device__ __forceinline__ f32x4 coherent_load16(__amdgpu_buffer_rsrc_t r, int byte_off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, kSc1);
 }
 __device__ __forceinline__ void coherent_store2(float* p, float a, float b) {
   typedef unsigned long long u64;
   typedef float f32x2 __attribute__((ext_vector_type(2)));
   __hip_atomic_store((u64*)p, __builtin_bit_cast(u64, f32x2{a, b}), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ f32x4 coherent_load4(const float* p) {
-  typedef unsigned long long u64;
-  typedef float f32x2 __attribute__((ext_vector_type(2)));
-  const f32x2 lo = __builtin_bit_cast(f32x2, __hip_atomic_load((u64*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-  const f32x2 hi =
-      __builtin_bit_cast(f32x2, __hip_atomic_load((u64*)p + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-  return f32x4{lo[0], lo[1], hi[0], hi[1]};
 }
 __device__ __forceinline__ void coherent_load2(const float* p, float& a, float& b) {
   typedef unsigned long long u64;
@@ -236,27 +240,18 @@ __device__ __forceinline__ void fold_init(Fold<NP>& F) {
   }
 }
 
-template <int NP>
-__device__ __forceinline__ void fold_one(Fold<NP>& F, const float (&m)[NP], const float (&l)[NP],
-                                         const f32x4 (&x0)[NP], const f32x4 (&x1)[NP]) {
-#pragma unroll
-  for (int i = 0; i < NP; ++i) {
-    const float M2 = fmaxf(F.M[i], m[i]);
-    const float c_old = __builtin_amdgcn_exp2f(F.M[i] - M2);
-    const float c_new = l[i] * __builtin_amdgcn_exp2f(m[i] - M2);
-    F.o0[i] = F.o0[i] * c_old + x0[i] * c_new;
-    F.o1[i] = F.o1[i] * c_old + x1[i] * c_new;
-    F.L[i] = F.L[i] * c_old + c_new;
-    F.M[i] = M2;
-  }
-}
-
-// Fold records 0 .. n-1 in order.  rec(u, m, l, x0, x1) fetches record u's
-// values for every pair of the lane; the fetches of kRound records are
-// issued before any of them is folded.
+// Fold records 0 .. n-1 (n the same for the whole wave) in order.
+// rec(u, m, l, x0, x1) fetches record u's values for every pair of the lane;
+// the fetches of kRound records are issued before any of them is folded.
+// Per round: the new maximum first, then one exponential per record and
+// o += w x as fused multiply-adds in record order (the running sums are
+// rescaled once per round, not once per record).  The order of the sums is
+// fixed by the record indices, so the fold is bit-identical whichever wave
+// performs it.
 template <int NP, class Rec>
 __device__ __forceinline__ void fold_records(Fold<NP>& F, int n, Rec rec) {
   constexpr int R = kRound<NP>;
+  n = __builtin_amdgcn_readfirstlane(n);
   for (int r0 = 0; r0 < n; r0 += R) {
     float m[R][NP], l[R][NP];
     f32x4 x0[R][NP], x1[R][NP];
@@ -264,8 +259,31 @@ __device__ __forceinline__ void fold_records(Fold<NP>& F, int n, Rec rec) {
     for (int u = 0; u < R; ++u)
       if (r0 + u < n) rec(r0 + u, m[u], l[u], x0[u], x1[u]);
 #pragma unroll
-    for (int u = 0; u < R; ++u)
-      if (r0 + u < n) fold_one<NP>(F, m[u], l[u], x0[u], x1[u]);
+    for (int i = 0; i < NP; ++i) {
+      float M2 = F.M[i];
+#pragma unroll
+      for (int u = 0; u < R; ++u)
+        if (r0 + u < n) M2 = fmaxf(M2, m[u][i]);
+      if (r0 > 0) {  // the sums so far move to the new maximum
+        const float c = __builtin_amdgcn_exp2f(F.M[i] - M2);
+        F.o0[i] *= c;
+        F.o1[i] *= c;
+        F.L[i] *= c;
+      }
+#pragma unroll
+      for (int u = 0; u < R; ++u) {
+        if (r0 + u < n) {
+          const float wgt = l[u][i] * __builtin_amdgcn_exp2f(m[u][i] - M2);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            F.o0[i][e] = __builtin_fmaf(x0[u][i][e], wgt, F.o0[i][e]);
+            F.o1[i][e] = __builtin_fmaf(x1[u][i][e], wgt, F.o1[i][e]);
+          }
+          F.L[i] += wgt;
+        }
+      }
+      F.M[i] = M2;
+    }
   }
 }
 
@@ -309,9 +327,10 @@ __device__ __forceinline__ void fetch_record(const DecodeArgs& a, size_t slot, c
       x1[i] = *(const f32x4*)(own + nn * 1024 + (hd + 16 * (q + 1)) * 16);
     } else {
       coherent_load2(a.rec_ml + (slot * G + hd) * 2, m[i], l[i]);
-      const float* ro = a.rec_o + (slot * G + hd) * kHeadDim + d0;
-      x0[i] = coherent_load4(ro);
-      x1[i] = coherent_load4(ro + 4);
+      const __amdgpu_buffer_rsrc_t r = record_rsrc(a.rec_o, slot, G);
+      const int bo = (hd * kHeadDim + d0) * 4;
+      x0[i] = coherent_load16(r, bo);
+      x1[i] = coherent_load16(r, bo + 16);
     }
   }
 }
@@ -353,9 +372,10 @@ __device__ __forceinline__ void write_record(const DecodeArgs& a, const Pairs<NP
 #pragma unroll
   for (int i = 0; i < NP; ++i) {
     if (!P.ok[i]) continue;
-    float* ro = a.rec_o + (dst * G + P.hd[i]) * kHeadDim + P.d0[i];
-    coherent_store4(ro, x0[i]);
-    coherent_store4(ro + 4, x1[i]);
+    const __amdgpu_buffer_rsrc_t r = record_rsrc(a.rec_o, dst, G);
+    const int bo = (P.hd[i] * kHeadDim + P.d0[i]) * 4;
+    coherent_store16(r, bo, x0[i]);
+    coherent_store16(r, bo + 16, x1[i]);
     if (P.d0[i] == 0) coherent_store2(a.rec_ml + (dst * G + P.hd[i]) * 2, m[i], l[i]);
   }
 }
@@ -567,8 +587,9 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       const size_t d = ((size_t)dhi << 32) | dlo;
       if (li >= G) continue;
       if (kind == 2) {  // partial record, slot d
-        float* ro = a.rec_o + (d * G + li) * kHeadDim;
-        for (int nn = 0; nn < 8; ++nn) coherent_store4(ro + 16 * nn + 4 * lj, *(const f32x4*)(base + nn * 1024 + lane * 16));
+        const __amdgpu_buffer_rsrc_t r = record_rsrc(a.rec_o, d, G);
+        for (int nn = 0; nn < 8; ++nn)
+          coherent_store16(r, (li * kHeadDim + 16 * nn + 4 * lj) * 4, *(const f32x4*)(base + nn * 1024 + lane * 16));
         if (lj == 0) {
           const float* ml = (const float*)(base + 8192 + lane * 8);
           coherent_store2(a.rec_ml + (d * G + li) * 2, ml[0], ml[1]);
@@ -828,8 +849,9 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   };
   auto seg_info = [&](int s, int g) __attribute__((always_inline)) {
     SegInfo f;
-    const int nus = pre[s + 1] - pre[s];
-    const int a0 = Hkv * pre[s] + g * nus;  // first unit of the segment in the stream
+    // the same for the whole wave: scalar registers, scalar branches
+    const int nus = __builtin_amdgcn_readfirstlane(pre[s + 1] - pre[s]);
+    const int a0 = __builtin_amdgcn_readfirstlane(Hkv * pre[s] + g * nus);  // first unit of the segment in the stream
     f.k0 = a0 / C;
     f.kend = (a0 + nus - 1) / C;
     f.np = f.kend - f.k0 + 1;
@@ -888,6 +910,12 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   // The last arrival of a group merges it.  One pass over the records covers
   // every (head, 8-value chunk) pair of the GQA group: two pairs per lane up
   // to 8 heads, four up to 16.
+  // A counter is returned to zero by its last arrival, after this wave's
+  // merges: no other wave touches it again in this launch, and a store ahead
+  // of the record loads would make their wait include the store's
+  // write-through (a wave's memory counter retires loads and stores in issue
+  // order).  Bit x: group counter of piece x; bit 2 + x: its segment counter.
+  unsigned rezero = 0;
   auto merge_pieces = [&](auto np_c) __attribute__((always_inline)) {
     constexpr int NP = decltype(np_c)::value;
     const Pairs<NP> P = pairs_of<NP>(lane, G * 16);
@@ -903,7 +931,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       };
       if (!mine && __shfl(x == 0 ? old0 : old1, 0) != f.gn - 1) continue;  // not the group's last arrival
       asm volatile("" ::: "memory");  // record loads are issued after this branch resolves
-      if (lane == 0) __hip_atomic_store(group_cnt(f.kg), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      rezero |= 1u << x;
       // the group's pieces, in order (this wave's own piece from LDS)
       const int own_idx = mine ? f.r - f.gfirst : -1;
       Fold<NP> Fg;
@@ -934,7 +962,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       const int c_own = f.gfirst / kFanIn;
       if (__shfl(done, 0) == f.ngroups - 1) {
         asm volatile("" ::: "memory");  // group record loads are issued after this branch resolves
-        if (lane == 0) __hip_atomic_store(seg_cnt(f.kend), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        rezero |= 4u << x;
         Fold<NP> F;
         fold_init(F);
         fold_records(F, f.ngroups, [&](int u, float(&m)[NP], float(&l)[NP], f32x4(&x0)[NP], f32x4(&x1)[NP])
@@ -960,7 +988,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       if (lane == 0) old = __hip_atomic_fetch_add(seg_cnt(f.kend), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (__shfl(old, 0) != f.ngroups - 1) continue;
       asm volatile("" ::: "memory");
-      if (lane == 0) __hip_atomic_store(seg_cnt(f.kend), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      rezero |= 4u << x;
       Fold<NP> F;
       fold_init(F);
       fold_records(F, f.ngroups, [&](int u, float(&m)[NP], float(&l)[NP], f32x4(&x0)[NP], f32x4(&x1)[NP])
@@ -974,6 +1002,12 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     merge_pieces(std::integral_constant<int, 4>{});
   else
     merge_pieces(std::integral_constant<int, 2>{});
+  if (lane == 0) {
+    if (rezero & 1u) __hip_atomic_store(group_cnt(f0.kg), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (rezero & 2u) __hip_atomic_store(group_cnt(f1.kg), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (rezero & 4u) __hip_atomic_store(seg_cnt(f0.kend), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (rezero & 8u) __hip_atomic_store(seg_cnt(f1.kend), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
 }
 
 template __global__ void paged_decode_kernel<false>(DecodeArgs);

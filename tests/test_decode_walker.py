@@ -257,9 +257,12 @@ def run_merge_protocol(sim, rng, p_staged=0.8):
     Per wave, as the kernel orders it: read both group counters (atomic
     loads) for pieces whose record is still staged in LDS; publish and count
     the pieces that were not found to be the group's last; then, piece by
-    piece, the group's last arrival merges the group (resetting its counter)
-    and either writes the segment or goes through the segment counter (load,
-    then group record and increment unless every other group is done)."""
+    piece, the group's last arrival merges the group and either writes the
+    segment or goes through the segment counter (load, then group record and
+    increment unless every other group is done); last, after a step of its
+    own, the wave returns to zero every counter it was the last arrival of.
+    No wave may read or count a counter between its last arrival and that
+    reset."""
     C, pre = sim["C"], sim["pre"]
     hkv = sim["hkv"]
     seg_of_piece = {}
@@ -279,6 +282,11 @@ def run_merge_protocol(sim, rng, p_staged=0.8):
             waves.setdefault(w, []).append(info)
     group_cnt, seg_cnt = {}, {}
     published, group_published, written = set(), set(), {}
+    done_group, done_seg = set(), set()  # counters whose last arrival has come, not yet reset
+
+    def read(cnt, done, k):
+        assert k not in done, f"counter {k} read after its last arrival"
+        return cnt.get(k, 0)
 
     def merge_group(info, own):
         seg = info["seg"]
@@ -286,7 +294,7 @@ def run_merge_protocol(sim, rng, p_staged=0.8):
             r = info["gfirst"] + u
             if not (own and r == info["r"]):
                 assert (seg, r) in published, f"merge of {seg} read piece {r} before it was published"
-        group_cnt[info["kg"]] = 0
+        done_group.add(info["kg"])
 
     def steps_of(w):
         pieces = sorted(waves[w], key=lambda i: i["r"] != 0)  # the slice's first piece, then its last
@@ -295,44 +303,53 @@ def run_merge_protocol(sim, rng, p_staged=0.8):
         # 1. atomic loads of the group counters (records still in LDS)
         for x, info in enumerate(pieces):
             if staged[x]:
-                mine[x] = group_cnt.get(info["kg"], 0) == info["gn"] - 1
+                mine[x] = read(group_cnt, done_group, info["kg"]) == info["gn"] - 1
         yield
         # 2. publish and count the others
         last = [False] * len(pieces)
         for x, info in enumerate(pieces):
             if not mine[x]:
                 published.add((info["seg"], info["r"]))
-                old = group_cnt.get(info["kg"], 0)
+                old = read(group_cnt, done_group, info["kg"])
                 group_cnt[info["kg"]] = old + 1
                 last[x] = old == info["gn"] - 1
                 yield
         # 3. merges
+        resets = []
         for x, info in enumerate(pieces):
             if not (mine[x] or last[x]):
                 continue
             merge_group(info, mine[x])
+            resets.append((group_cnt, done_group, info["kg"]))
             yield
             seg = info["seg"]
             if info["ngroups"] == 1:
                 written[seg] = written.get(seg, 0) + 1
                 continue
             c_own = info["gfirst"] // FAN_IN
-            if seg_cnt.get(info["kend"], 0) == info["ngroups"] - 1:
+            if read(seg_cnt, done_seg, info["kend"]) == info["ngroups"] - 1:
                 for c in range(info["ngroups"]):
                     if c != c_own:
                         assert (seg, c) in group_published, f"{seg}: group {c} read before it was published"
-                seg_cnt[info["kend"]] = 0
+                done_seg.add(info["kend"])
+                resets.append((seg_cnt, done_seg, info["kend"]))
                 written[seg] = written.get(seg, 0) + 1
                 continue
             group_published.add((seg, c_own))
-            old = seg_cnt.get(info["kend"], 0)
+            old = read(seg_cnt, done_seg, info["kend"])
             seg_cnt[info["kend"]] = old + 1
             yield
             if old == info["ngroups"] - 1:
                 for c in range(info["ngroups"]):
                     assert (seg, c) in group_published
-                seg_cnt[info["kend"]] = 0
+                done_seg.add(info["kend"])
+                resets.append((seg_cnt, done_seg, info["kend"]))
                 written[seg] = written.get(seg, 0) + 1
+        # 4. the counters this wave was the last arrival of return to zero
+        yield
+        for cnt, done, k in resets:
+            cnt[k] = 0
+            done.discard(k)
 
     live = {w: steps_of(w) for w in waves}
     while live:
@@ -343,6 +360,7 @@ def run_merge_protocol(sim, rng, p_staged=0.8):
             del live[w]
     assert written == {seg: 1 for seg in sim["pieces"]}, "a cut segment was written other than once"
     assert all(v == 0 for v in group_cnt.values()) and all(v == 0 for v in seg_cnt.values())
+    assert not done_group and not done_seg
 
 
 @pytest.mark.parametrize("trial", range(30))
