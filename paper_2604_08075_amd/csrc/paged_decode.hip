@@ -391,6 +391,12 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   constexpr int UB = GE::UB, UT = GE::UT, TILE = GE::TILE, NZ = GE::NZ;
   __shared__ int tiles_lds[kWaves][kMaxUnitsPerWave * UB];
   __shared__ int wave_sums[kWaves];
+  // Segments cut only between this workgroup's own slices are merged here:
+  // arrivals per first wave of such a segment, and where each wave's split
+  // pieces' records are (byte offset in its staging area, or -1: in their
+  // global slot).
+  __shared__ int wg_cnt[kWaves];
+  __shared__ int wg_dir[kWaves][2];
   __shared__ __attribute__((aligned(16))) char stage_lds[kWaves][kStageBytes];
   __shared__ long long stage_dst[kWaves][kMaxStaged];  // element offset of a row in `out`, or a record slot
   __shared__ int stage_kind[kWaves][kMaxStaged];       // 0 bf16 row, 1 fp32 row, 2 record
@@ -431,6 +437,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       if (lane >= off) incl += v;
     }
     if (lane == 63) wave_sums[w] = incl;
+    if (tid < kWaves) wg_cnt[tid] = 0;
     __syncthreads();
     int run = incl - local;
     for (int k = 0; k < w; ++k) run += wave_sums[k];
@@ -870,6 +877,16 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   SegInfo f0 = {}, f1 = {};
   if (arr_s0 >= 0) f0 = seg_info(arr_s0, arr_g0);
   if (arr_s1 >= 0) f1 = seg_info(arr_s1, arr_g1);
+  // A segment whose pieces all lie in this workgroup's slices is merged
+  // inside it: its pieces are counted on an LDS counter and read from their
+  // owners' staging areas, with no global record, no device-wide atomic and
+  // no counter to reset.  The fold is the same, in the same order, so the
+  // bits are those of the global path.
+  const int wg_first = gw - w;  // first wave of this workgroup
+  const bool in0 = arr_s0 >= 0 && f0.k0 >= wg_first && f0.kend < wg_first + kWaves;
+  const bool in1 = arr_s1 >= 0 && f1.k0 >= wg_first && f1.kend < wg_first + kWaves;
+  const bool gl0 = arr_s0 >= 0 && !in0;  // pieces that go through the device-wide protocol
+  const bool gl1 = arr_s1 >= 0 && !in1;
   // If a group counter already shows every other piece of the group (read
   // with an atomic load, far quicker than an increment's round trip), this
   // wave is that group's last arrival: it merges with its own partial
@@ -877,35 +894,81 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   // increment.  Both counters are read together.
   int c0 = 0, c1 = 0;
   if (lane == 0) {
-    if (ent0 >= 0) c0 = __hip_atomic_load(group_cnt(f0.kg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (ent1 >= 0) c1 = __hip_atomic_load(group_cnt(f1.kg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (gl0 && ent0 >= 0) c0 = __hip_atomic_load(group_cnt(f0.kg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (gl1 && ent1 >= 0) c1 = __hip_atomic_load(group_cnt(f1.kg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  const bool mine0 = ent0 >= 0 && __shfl(c0, 0) == f0.gn - 1;
-  const bool mine1 = ent1 >= 0 && __shfl(c1, 0) == f1.gn - 1;
+  const bool mine0 = gl0 && ent0 >= 0 && __shfl(c0, 0) == f0.gn - 1;
+  const bool mine1 = gl1 && ent1 >= 0 && __shfl(c1, 0) == f1.gn - 1;
   // Records first: they must have reached the coherence point before their
   // arrivals are counted.  Finished rows go out after the counters, their
-  // stores overlapping the atomics' round trip.
-  flush((mine0 ? 1u << ent0 : 0u) | (mine1 ? 1u << ent1 : 0u), 1);
+  // stores overlapping the atomics' round trip.  Records merged from LDS
+  // (this wave's last arrivals, and pieces of segments inside the
+  // workgroup) stay in the staging area.
+  flush(((mine0 || in0) && ent0 >= 0 ? 1u << ent0 : 0u) | ((mine1 || in1) && ent1 >= 0 ? 1u << ent1 : 0u), 1);
   int old0 = 0, old1 = 0;
-  auto entry_ptr = [&](int e) __attribute__((always_inline)) {
-    return e >= 0 ? stg + (__builtin_amdgcn_readfirstlane(stage_kind[w][e]) >> 4) : nullptr;
+  auto rec0_offset = [&](int e) __attribute__((always_inline)) {
+    return __builtin_amdgcn_readfirstlane(stage_kind[w][e]) >> 4;  // byte offset of entry e in the staging area
   };
+  auto entry_ptr = [&](int e) __attribute__((always_inline)) { return e >= 0 ? stg + rec0_offset(e) : nullptr; };
   const char* const rec0 = entry_ptr(ent0);
   const char* const rec1 = entry_ptr(ent1);
-  if ((arr_s0 >= 0 && !mine0) || (arr_s1 >= 0 && !mine1)) {
+  if ((gl0 && !mine0) || (gl1 && !mine1) || (in0 && ent0 < 0) || (in1 && ent1 < 0)) {
     // this wave's record stores have completed (at the coherence point)
     // before it counts them
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     // Both pieces' arrivals are counted before either count is examined:
     // a device-wide atomic takes a few microseconds to return, and the two
     // would otherwise follow one another.
-    if (arr_s0 >= 0 && !mine0 && lane == 0)
+    if (gl0 && !mine0 && lane == 0)
       old0 = __hip_atomic_fetch_add(group_cnt(f0.kg), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (arr_s1 >= 0 && !mine1 && lane == 0)
+    if (gl1 && !mine1 && lane == 0)
       old1 = __hip_atomic_fetch_add(group_cnt(f1.kg), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   flush(0u, 2);
-  if (arr_s0 < 0 && arr_s1 < 0) return;
+  if (in0 || in1) {
+    // Publish where each piece's record is, then count it (release: the
+    // directory entry is visible before the count); the last arrival
+    // (acquire) folds the segment's pieces in order and writes its rows.
+    int lold0 = 0, lold1 = 0;
+    if (lane == 0) {
+      if (in0) {
+        wg_dir[w][0] = ent0 >= 0 ? (int)(rec0_offset(ent0)) : -1;
+        lold0 = __hip_atomic_fetch_add(&wg_cnt[f0.k0 - wg_first], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
+      }
+      if (in1) {
+        wg_dir[w][1] = ent1 >= 0 ? (int)(rec0_offset(ent1)) : -1;
+        lold1 = __hip_atomic_fetch_add(&wg_cnt[f1.k0 - wg_first], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
+      }
+    }
+    const bool last0 = in0 && __shfl(lold0, 0) == f0.np - 1;
+    const bool last1 = in1 && __shfl(lold1, 0) == f1.np - 1;
+    if (last0 || last1) {
+      asm volatile("" ::: "memory");  // record reads are issued after this branch resolves
+      auto merge_local = [&](auto np_c, const SegInfo& f, int s, int g) __attribute__((always_inline)) {
+        constexpr int NP = decltype(np_c)::value;
+        const Pairs<NP> P = pairs_of<NP>(lane, G * 16);
+        Fold<NP> F;
+        fold_init(F);
+        fold_records(F, f.np, [&](int r, float(&m)[NP], float(&l)[NP], f32x4(&x0)[NP], f32x4(&x1)[NP])
+                                  __attribute__((always_inline)) {
+                                    const int slot = r == 0 ? f.first_slot : 2 * (f.k0 + r);
+                                    const int ow = __builtin_amdgcn_readfirstlane((slot >> 1) - wg_first);
+                                    const int d = __builtin_amdgcn_readfirstlane(wg_dir[ow][slot & 1]);
+                                    fetch_record(a, (size_t)slot, d >= 0 ? (const char*)stage_lds[ow] + d : nullptr,
+                                                 P, m, l, x0, x1);
+                                  });
+        write_rows(a, F, P, s, g);
+      };
+      for (int x = 0; x < 2; ++x) {
+        if (!(x == 0 ? last0 : last1)) continue;
+        const SegInfo f = x == 0 ? f0 : f1;
+        const int s = x == 0 ? arr_s0 : arr_s1, g = x == 0 ? arr_g0 : arr_g1;
+        if (G > 8) merge_local(std::integral_constant<int, 4>{}, f, s, g);
+        else merge_local(std::integral_constant<int, 2>{}, f, s, g);
+      }
+    }
+  }
+  if (!gl0 && !gl1) return;
 
   // The last arrival of a group merges it.  One pass over the records covers
   // every (head, 8-value chunk) pair of the GQA group: two pairs per lane up
@@ -921,7 +984,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     const Pairs<NP> P = pairs_of<NP>(lane, G * 16);
     for (int x = 0; x < 2; ++x) {
       const int s = x == 0 ? arr_s0 : arr_s1;
-      if (s < 0) continue;
+      if (s < 0 || (x == 0 ? in0 : in1)) continue;
       const int g = x == 0 ? arr_g0 : arr_g1;
       const bool mine = x == 0 ? mine0 : mine1;
       const char* const own_rec = x == 0 ? rec0 : rec1;
@@ -1124,11 +1187,12 @@ int validate(const dp_decode_shape* sh, Plan* plan) {
   plan->unit_tokens = unit;
   plan->min_chunk = P ? P / unit : 1;
   // LDS per workgroup: the kernel's static arrays (tile lists, wave sums,
-  // staging of finished rows and records, with 256 bytes for alignment) +
+  // staging of finished rows and records, the workgroup's merge counters and
+  // record directory, with 256 bytes for alignment) +
   // unit prefix, context lengths and fp8 scales (dynamic)
   const size_t stat = (size_t)kWaves * kMaxUnitsPerWave * (fp8 ? 4 : 2) * sizeof(int) + kWaves * sizeof(int) +
                       (size_t)kWaves * kStageBytes + (size_t)kWaves * kMaxStaged * (sizeof(long long) + sizeof(int)) +
-                      256;
+                      (size_t)kWaves * 3 * sizeof(int) + 256;
   plan->dyn_lds = (size_t)(2 * sh->batch + 1 + 2 * sh->n_kv_heads) * 4;
   if (stat + plan->dyn_lds > kLdsBytes)
     return fail(DP_ENOTSUP, "paged_decode: %zu bytes of LDS per workgroup", stat + plan->dyn_lds);

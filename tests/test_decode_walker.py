@@ -256,7 +256,10 @@ def run_merge_protocol(sim, rng, p_staged=0.8):
 
     Per wave, as the kernel orders it: read both group counters (atomic
     loads) for pieces whose record is still staged in LDS; publish and count
-    the pieces that were not found to be the group's last; then, piece by
+    the pieces that were not found to be the group's last; count the pieces
+    of segments that lie inside one workgroup on that workgroup's counter
+    (their last arrival writes the segment, and they touch no global
+    counter); then, piece by
     piece, the group's last arrival merges the group and either writes the
     segment or goes through the segment counter (load, then group record and
     increment unless every other group is done); last, after a step of its
@@ -276,12 +279,13 @@ def run_merge_protocol(sim, rng, p_staged=0.8):
             gfirst = r - r % FAN_IN
             gn = min(np_, gfirst + FAN_IN) - gfirst
             info = dict(seg=(s, g), r=r, gfirst=gfirst, gn=gn, kg=k0 + gfirst + gn - 1, ngroups=-(-np_ // FAN_IN),
-                        kend=kend, np=np_)
+                        kend=kend, np=np_, k0=k0, local=k0 // WAVES == kend // WAVES)
             w = k0 + r
             seg_of_piece[(w, r == 0)] = info
             waves.setdefault(w, []).append(info)
-    group_cnt, seg_cnt = {}, {}
+    group_cnt, seg_cnt, wg_cnt = {}, {}, {}
     published, group_published, written = set(), set(), {}
+    published_local = set()  # pieces of segments merged inside their workgroup
     done_group, done_seg = set(), set()  # counters whose last arrival has come, not yet reset
 
     def read(cnt, done, k):
@@ -300,24 +304,41 @@ def run_merge_protocol(sim, rng, p_staged=0.8):
         pieces = sorted(waves[w], key=lambda i: i["r"] != 0)  # the slice's first piece, then its last
         staged = [bool(rng.random() < p_staged) for _ in pieces]
         mine = [False] * len(pieces)
-        # 1. atomic loads of the group counters (records still in LDS)
+        # 1. atomic loads of the group counters (records still in LDS); pieces
+        # of segments inside one workgroup take no part in the global protocol
         for x, info in enumerate(pieces):
-            if staged[x]:
+            if staged[x] and not info["local"]:
                 mine[x] = read(group_cnt, done_group, info["kg"]) == info["gn"] - 1
         yield
         # 2. publish and count the others
         last = [False] * len(pieces)
         for x, info in enumerate(pieces):
-            if not mine[x]:
+            if not mine[x] and not info["local"]:
                 published.add((info["seg"], info["r"]))
                 old = read(group_cnt, done_group, info["kg"])
                 group_cnt[info["kg"]] = old + 1
                 last[x] = old == info["gn"] - 1
                 yield
+        # 2b. segments inside the workgroup: publish the record's place, count
+        # on the workgroup's counter (keyed by the segment's first wave); the
+        # last arrival folds every piece and writes the segment
+        for x, info in enumerate(pieces):
+            if not info["local"]:
+                continue
+            seg = info["seg"]
+            published_local.add((seg, info["r"]))
+            key = (info["k0"] // WAVES, info["k0"])
+            old = wg_cnt.get(key, 0)
+            wg_cnt[key] = old + 1
+            if old == info["np"] - 1:
+                for r in range(info["np"]):
+                    assert (seg, r) in published_local, f"local merge of {seg} read piece {r} before it was published"
+                written[seg] = written.get(seg, 0) + 1
+            yield
         # 3. merges
         resets = []
         for x, info in enumerate(pieces):
-            if not (mine[x] or last[x]):
+            if info["local"] or not (mine[x] or last[x]):
                 continue
             merge_group(info, mine[x])
             resets.append((group_cnt, done_group, info["kg"]))
@@ -361,6 +382,10 @@ def run_merge_protocol(sim, rng, p_staged=0.8):
     assert written == {seg: 1 for seg in sim["pieces"]}, "a cut segment was written other than once"
     assert all(v == 0 for v in group_cnt.values()) and all(v == 0 for v in seg_cnt.values())
     assert not done_group and not done_seg
+    # every local counter saw exactly its segment's pieces (no reset needed:
+    # the counters live in LDS for one launch)
+    for (wg, k0), v in wg_cnt.items():
+        assert v == next(i["np"] for ws in waves.values() for i in ws if i["k0"] == k0 and i["local"])
 
 
 @pytest.mark.parametrize("trial", range(30))
