@@ -906,10 +906,10 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   // workgroup) stay in the staging area.
   flush(((mine0 || in0) && ent0 >= 0 ? 1u << ent0 : 0u) | ((mine1 || in1) && ent1 >= 0 ? 1u << ent1 : 0u), 1);
   int old0 = 0, old1 = 0;
-  auto rec0_offset = [&](int e) __attribute__((always_inline)) {
+  auto entry_offset = [&](int e) __attribute__((always_inline)) {
     return __builtin_amdgcn_readfirstlane(stage_kind[w][e]) >> 4;  // byte offset of entry e in the staging area
   };
-  auto entry_ptr = [&](int e) __attribute__((always_inline)) { return e >= 0 ? stg + rec0_offset(e) : nullptr; };
+  auto entry_ptr = [&](int e) __attribute__((always_inline)) { return e >= 0 ? stg + entry_offset(e) : nullptr; };
   const char* const rec0 = entry_ptr(ent0);
   const char* const rec1 = entry_ptr(ent1);
   if ((gl0 && !mine0) || (gl1 && !mine1) || (in0 && ent0 < 0) || (in1 && ent1 < 0)) {
@@ -932,11 +932,11 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     int lold0 = 0, lold1 = 0;
     if (lane == 0) {
       if (in0) {
-        wg_dir[w][0] = ent0 >= 0 ? (int)(rec0_offset(ent0)) : -1;
+        wg_dir[w][0] = ent0 >= 0 ? (int)(entry_offset(ent0)) : -1;
         lold0 = __hip_atomic_fetch_add(&wg_cnt[f0.k0 - wg_first], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
       }
       if (in1) {
-        wg_dir[w][1] = ent1 >= 0 ? (int)(rec0_offset(ent1)) : -1;
+        wg_dir[w][1] = ent1 >= 0 ? (int)(entry_offset(ent1)) : -1;
         lold1 = __hip_atomic_fetch_add(&wg_cnt[f1.k0 - wg_first], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
       }
     }
