@@ -104,6 +104,7 @@ def simulate(ctx, hkv, fp8, max_ctx, max_blocks_per_seq, partition_tokens=0, wgs
     q_rows, bt_reads, computed = [], [], []
     records = {}        # record slot -> (s, g, piece index r)
     pieces = {}         # (s, g) -> list of (wave, slot)
+    staged = {}         # wave -> its staging entries in order: ("row", None) or ("rec", slot)
     for gw in range(TW):
         u0 = gw * C
         u1 = min(u0 + C, U)
@@ -137,8 +138,10 @@ def simulate(ctx, hkv, fp8, max_ctx, max_blocks_per_seq, partition_tokens=0, wgs
             if not (seg_end or ui == n - 1):
                 return
             if state["piece_j0"] == 0 and seg_end:
-                return  # whole segment: written straight to the output
+                staged.setdefault(gw, []).append(("row", None))
+                return  # whole segment: its rows, staged then written to the output
             slot = 2 * gw + (0 if state["piece_first"] else 1)
+            staged.setdefault(gw, []).append(("rec", slot))
             assert slot not in records
             records[slot] = (cs.s, cs.g)
             pieces.setdefault((cs.s, cs.g), []).append((gw, slot))
@@ -161,7 +164,25 @@ def simulate(ctx, hkv, fp8, max_ctx, max_blocks_per_seq, partition_tokens=0, wgs
             ui += 1
         compute(ui, cs)
     return dict(B=B, TW=TW, C=C, U=U, pre=pre, q_rows=q_rows, bt_reads=bt_reads, computed=computed,
-                records=records, pieces=pieces, max_blocks_per_seq=max_blocks_per_seq)
+                records=records, pieces=pieces, max_blocks_per_seq=max_blocks_per_seq, staged=staged)
+
+
+STAGE_BYTES, MAX_STAGED = 24 * 1024, 6      # a wave's LDS staging area: bytes and entries
+ROW_BYTES, REC_BYTES = 4096, 8192 + 512     # one (sequence, KV head)'s bf16 rows; one record (o, m, l)
+
+
+def flushed_mid_loop(entries, row_bytes=ROW_BYTES):
+    """Record slots a wave's staging writes out before its slice ends: the
+    kernel flushes every staged entry when the next one would not fit."""
+    out, st_n, st_off, pending = set(), 0, 0, []
+    for kind, slot in entries:
+        size = row_bytes if kind == "row" else REC_BYTES
+        if st_n == MAX_STAGED or st_off + size > STAGE_BYTES:
+            out |= {x for x in pending if x is not None}
+            st_n, st_off, pending = 0, 0, []
+        st_n, st_off = st_n + 1, st_off + size
+        pending.append(slot)
+    return out
 
 
 def check(sim, hkv):
@@ -386,6 +407,36 @@ def run_merge_protocol(sim, rng, p_staged=0.8):
     # the counters live in LDS for one launch)
     for (wg, k0), v in wg_cnt.items():
         assert v == next(i["np"] for ws in waves.values() for i in ws if i["k0"] == k0 and i["local"])
+
+
+@pytest.mark.parametrize("fp8", [False, True])
+def test_largest_batch_reaches_both_local_merge_sources(fp8):
+    """The GPU test of the largest batch (4,096 short contexts, 2 KV heads)
+    merges segments cut inside one workgroup from both places a piece's record
+    can be: still in its owner's LDS staging area, and in its global slot after
+    a mid-loop flush.  Replays that batch's slices and staging here."""
+    rng = np.random.default_rng(31)
+    ctx = rng.integers(0, 97, 4096)
+    ctx[rng.integers(0, 4096, 64)] = 0
+    sim = simulate(list(ctx), 2, fp8, int(ctx.max()), 8)  # the workload's max_context_len and table width
+    check(sim, 2)
+    flushed = set()
+    for entries in sim["staged"].values():
+        flushed |= flushed_mid_loop(entries)
+    C, pre = sim["C"], sim["pre"]
+    in_lds = in_slot = 0
+    for (s_, g), got in sim["pieces"].items():
+        nus = pre[s_ + 1] - pre[s_]
+        a0 = 2 * pre[s_] + g * nus
+        k0, kend = a0 // C, (a0 + nus - 1) // C
+        if k0 // WAVES != kend // WAVES:
+            continue
+        for _, slot in got:
+            if slot in flushed:
+                in_slot += 1
+            else:
+                in_lds += 1
+    assert in_lds > 0 and in_slot > 0, (in_lds, in_slot)
 
 
 @pytest.mark.parametrize("trial", range(30))
