@@ -295,10 +295,11 @@ int32_t paged_decode_partition_tokens(const dp_decode_shape* shape);
  *
  * Split-K over the context: the cached tokens of all (sequence, KV head)
  * pairs are cut into equal slices, one per wave; a pair cut by slice
- * boundaries leaves per-slice softmax partials (o_p, m_p, l_p) in the
- * workspace (or in the workgroup's LDS when all its slices run in one
- * workgroup), which the last slice to finish merges with log-sum-exp weights
- * M = max_p m_p, w_p = l_p * 2^(m_p - M), out = sum_p w_p o_p / sum_p w_p.
+ * boundaries leaves per-slice softmax partials (o_p, m_p, l_p), which are
+ * merged with log-sum-exp weights M = max_p m_p, w_p = l_p * 2^(m_p - M),
+ * out = sum_p w_p o_p / sum_p w_p: first inside each workgroup (through its
+ * LDS), then, for pairs whose slices span several workgroups, the
+ * workgroups' partials through the workspace, by the last to finish.
  * Results are deterministic: the same inputs and shape give the same bits. */
 int paged_decode_attention(const void* q, const void* k_blocks, const void* v_blocks,
                            const int32_t* block_tables, const int32_t* context_lens,

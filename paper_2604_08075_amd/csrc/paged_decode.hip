@@ -206,13 +206,18 @@ __device__ __forceinline__ void store_out8(const DecodeArgs& a, size_t off, f32x
   }
 }
 
-// Record slots: 2k and 2k + 1 hold the first and last split piece of wave k;
-// 2 * waves + k holds the merged record of the group of pieces whose last
-// piece is wave k's.  A record is (o, m, l): o normalised by l, m in log2
-// units.  Pieces are merged in groups of kFanIn consecutive pieces, then the
-// group records, so that a long segment cut into many pieces needs few
-// memory round trips on each level.
-constexpr int kFanIn = 8;
+// Records (o, m, l): o normalised by l, m in log2 units.  Slots 2k and
+// 2k + 1 hold the first and last split piece of wave k when a staging area
+// that fills up in the middle of a slice writes them out.  A segment cut by
+// slice boundaries is merged in two stages: first inside each workgroup
+// (through LDS), then across workgroups.  Slots 2 * waves + 2b and
+// 2 * waves + 2b + 1 hold workgroup b's first and last piece of segments that
+// cross its edges, and 2 * waves + 2 * workgroups + b the merged record of
+// the group of workgroup pieces whose last is workgroup b's.  Workgroup
+// pieces are merged in groups of kFanIn consecutive ones, then the group
+// records, so that a segment cut into many pieces needs few memory round
+// trips on each level.
+constexpr int kFanIn = 16;
 
 // Log-sum-exp fold of records, by one wave, in record order:
 // M = max_p m_p, w_p = l_p 2^(m_p - M), o = sum_p w_p o_p / sum_p w_p,
@@ -391,11 +396,11 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   constexpr int UB = GE::UB, UT = GE::UT, TILE = GE::TILE, NZ = GE::NZ;
   __shared__ int tiles_lds[kWaves][kMaxUnitsPerWave * UB];
   __shared__ int wave_sums[kWaves];
-  // Segments cut only between this workgroup's own slices are merged here:
-  // arrivals per first wave of such a segment, and where each wave's split
-  // pieces' records are (byte offset in its staging area, or -1: in their
-  // global slot).
-  __shared__ int wg_cnt[kWaves];
+  // Split pieces are first merged inside the workgroup: arrivals per share
+  // of a segment (keyed by the share's first piece: wave, first or last), and
+  // where each wave's split pieces' records are (byte offset in its staging
+  // area, or -1: in their wave slot).
+  __shared__ int wg_cnt[2 * kWaves];
   __shared__ int wg_dir[kWaves][2];
   __shared__ __attribute__((aligned(16))) char stage_lds[kWaves][kStageBytes];
   __shared__ long long stage_dst[kWaves][kMaxStaged];  // element offset of a row in `out`, or a record slot
@@ -437,7 +442,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       if (lane >= off) incl += v;
     }
     if (lane == 63) wave_sums[w] = incl;
-    if (tid < kWaves) wg_cnt[tid] = 0;
+    if (tid < 2 * kWaves) wg_cnt[tid] = 0;
     __syncthreads();
     int run = incl - local;
     for (int k = 0; k < w; ++k) run += wave_sums[k];
@@ -843,169 +848,165 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   }
   last(RA, qE, ui);
 
-  // ---- 5. signal split pieces; the last arrivers merge them ----
-  // Pieces are merged in groups of kFanIn consecutive pieces, then the groups.
-  // Piece r of a segment is wave k0 + r's; a group's counter and record slot
-  // belong to the wave of its last piece (whose piece is that wave's first).
+  // ---- 5. merge the split pieces ----
+  // Stage 1, inside the workgroup: each piece of a segment is counted on an
+  // LDS counter of the segment's share of this workgroup (keyed by the share's
+  // first piece), after its owner has noted where its record is: in its LDS
+  // staging area, or in its wave slot when a mid-loop flush wrote it out.  The
+  // last arrival folds the share's pieces in order.  A segment entirely inside
+  // the workgroup is then written; the share of a segment that crosses the
+  // workgroup's edges is the workgroup's piece for stage 2.
+  // Stage 2, across workgroups: workgroup pieces are merged in groups of
+  // kFanIn consecutive ones, then the groups, by the last arrival on
+  // device-wide counters (the workgroup of a group's last piece, of a
+  // segment's last piece).  The folds take records in a fixed order, so the
+  // result does not depend on which wave performs them.
   int* const group_base = a.arrivals;
   int* const seg_base = a.arrivals + TW;
   auto group_cnt = [&](int k) __attribute__((always_inline)) { return group_base + k; };
   auto seg_cnt = [&](int k) __attribute__((always_inline)) { return seg_base + k; };
-  struct SegInfo {
-    int k0, kend, np, first_slot, r, gfirst, gn, kg, ngroups;
+  const int wg_first = gw - w;          // first wave of this workgroup
+  const int nwg = (int)gridDim.x;
+  const int CW = kWaves * C;            // units per workgroup
+  const size_t rec_wg = (size_t)2 * TW;                // workgroup piece slots
+  const size_t rec_grp = rec_wg + (size_t)2 * nwg;     // group record slots
+  struct Part {
+    int s, g, k0, first_slot, pk0, pkend, key;         // the segment's waves; this workgroup's share of them
+    int bk0, bkend, nwp, first_wslot, rb, gfirst, gn, kg, ngroups;  // its workgroups
   };
-  auto seg_info = [&](int s, int g) __attribute__((always_inline)) {
-    SegInfo f;
+  auto part_of = [&](int s, int g) __attribute__((always_inline)) {
+    Part p;
     // the same for the whole wave: scalar registers, scalar branches
     const int nus = __builtin_amdgcn_readfirstlane(pre[s + 1] - pre[s]);
-    const int a0 = __builtin_amdgcn_readfirstlane(Hkv * pre[s] + g * nus);  // first unit of the segment in the stream
-    f.k0 = a0 / C;
-    f.kend = (a0 + nus - 1) / C;
-    f.np = f.kend - f.k0 + 1;
-    f.first_slot = 2 * f.k0 + (a0 > f.k0 * C ? 1 : 0);
-    f.r = gw - f.k0;
-    f.gfirst = f.r - f.r % kFanIn;
-    f.gn = min(f.np, f.gfirst + kFanIn) - f.gfirst;
-    f.kg = f.k0 + f.gfirst + f.gn - 1;
-    f.ngroups = (f.np + kFanIn - 1) / kFanIn;
-    return f;
+    const int a0 = __builtin_amdgcn_readfirstlane(Hkv * pre[s] + g * nus);  // first unit of the segment
+    p.s = s;
+    p.g = g;
+    p.k0 = a0 / C;
+    const int kend = (a0 + nus - 1) / C;
+    p.first_slot = 2 * p.k0 + (a0 > p.k0 * C ? 1 : 0);
+    p.pk0 = max(p.k0, wg_first);
+    p.pkend = min(kend, wg_first + kWaves - 1);
+    p.key = 2 * (p.pk0 - wg_first) + (p.pk0 == p.k0 ? (p.first_slot & 1) : 0);
+    p.bk0 = a0 / CW;
+    p.bkend = (a0 + nus - 1) / CW;
+    p.nwp = p.bkend - p.bk0 + 1;
+    p.first_wslot = 2 * p.bk0 + (a0 > p.bk0 * CW ? 1 : 0);
+    p.rb = (int)blockIdx.x - p.bk0;
+    p.gfirst = p.rb - p.rb % kFanIn;
+    p.gn = min(p.nwp, p.gfirst + kFanIn) - p.gfirst;
+    p.kg = p.bk0 + p.gfirst + p.gn - 1;
+    p.ngroups = (p.nwp + kFanIn - 1) / kFanIn;
+    return p;
   };
   // Piece x = 0 is the slice's first split piece, x = 1 its last.  The
   // staging entry of each, while its record is still in LDS:
   const int ent0 = own_x == 0 ? own_entry : first_entry;
   const int ent1 = own_x == 1 ? own_entry : -1;
-  SegInfo f0 = {}, f1 = {};
-  if (arr_s0 >= 0) f0 = seg_info(arr_s0, arr_g0);
-  if (arr_s1 >= 0) f1 = seg_info(arr_s1, arr_g1);
-  // A segment whose pieces all lie in this workgroup's slices is merged
-  // inside it: its pieces are counted on an LDS counter and read from their
-  // owners' staging areas, with no global record, no device-wide atomic and
-  // no counter to reset.  The fold is the same, in the same order, so the
-  // bits are those of the global path.
-  const int wg_first = gw - w;  // first wave of this workgroup
-  const bool in0 = arr_s0 >= 0 && f0.k0 >= wg_first && f0.kend < wg_first + kWaves;
-  const bool in1 = arr_s1 >= 0 && f1.k0 >= wg_first && f1.kend < wg_first + kWaves;
-  const bool gl0 = arr_s0 >= 0 && !in0;  // pieces that go through the device-wide protocol
-  const bool gl1 = arr_s1 >= 0 && !in1;
-  // If a group counter already shows every other piece of the group (read
-  // with an atomic load, far quicker than an increment's round trip), this
-  // wave is that group's last arrival: it merges with its own partial
-  // straight from LDS, with no record write, no wait for it and no
-  // increment.  Both counters are read together.
-  int c0 = 0, c1 = 0;
-  if (lane == 0) {
-    if (gl0 && ent0 >= 0) c0 = __hip_atomic_load(group_cnt(f0.kg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (gl1 && ent1 >= 0) c1 = __hip_atomic_load(group_cnt(f1.kg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  const bool mine0 = gl0 && ent0 >= 0 && __shfl(c0, 0) == f0.gn - 1;
-  const bool mine1 = gl1 && ent1 >= 0 && __shfl(c1, 0) == f1.gn - 1;
-  // Records first: they must have reached the coherence point before their
-  // arrivals are counted.  Finished rows go out after the counters, their
-  // stores overlapping the atomics' round trip.  Records merged from LDS
-  // (this wave's last arrivals, and pieces of segments inside the
-  // workgroup) stay in the staging area.
-  flush(((mine0 || in0) && ent0 >= 0 ? 1u << ent0 : 0u) | ((mine1 || in1) && ent1 >= 0 ? 1u << ent1 : 0u), 1);
-  int old0 = 0, old1 = 0;
+  Part p0 = {}, p1 = {};
+  if (arr_s0 >= 0) p0 = part_of(arr_s0, arr_g0);
+  if (arr_s1 >= 0) p1 = part_of(arr_s1, arr_g1);
+  // A record written out by a mid-loop flush has reached the coherence point
+  // before its piece is counted.
+  if ((arr_s0 >= 0 && ent0 < 0) || (arr_s1 >= 0 && ent1 < 0)) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  flush(0u, 2);  // finished rows; the pieces' records stay in the staging area
+  if (arr_s0 < 0 && arr_s1 < 0) return;
   auto entry_offset = [&](int e) __attribute__((always_inline)) {
     return __builtin_amdgcn_readfirstlane(stage_kind[w][e]) >> 4;  // byte offset of entry e in the staging area
   };
-  auto entry_ptr = [&](int e) __attribute__((always_inline)) { return e >= 0 ? stg + entry_offset(e) : nullptr; };
-  const char* const rec0 = entry_ptr(ent0);
-  const char* const rec1 = entry_ptr(ent1);
-  if ((gl0 && !mine0) || (gl1 && !mine1) || (in0 && ent0 < 0) || (in1 && ent1 < 0)) {
-    // this wave's record stores have completed (at the coherence point)
-    // before it counts them
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    // Both pieces' arrivals are counted before either count is examined:
-    // a device-wide atomic takes a few microseconds to return, and the two
-    // would otherwise follow one another.
-    if (gl0 && !mine0 && lane == 0)
-      old0 = __hip_atomic_fetch_add(group_cnt(f0.kg), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (gl1 && !mine1 && lane == 0)
-      old1 = __hip_atomic_fetch_add(group_cnt(f1.kg), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  flush(0u, 2);
-  if (in0 || in1) {
-    // Publish where each piece's record is, then count it (release: the
-    // directory entry is visible before the count); the last arrival
-    // (acquire) folds the segment's pieces in order and writes its rows.
-    int lold0 = 0, lold1 = 0;
-    if (lane == 0) {
-      if (in0) {
-        wg_dir[w][0] = ent0 >= 0 ? (int)(entry_offset(ent0)) : -1;
-        lold0 = __hip_atomic_fetch_add(&wg_cnt[f0.k0 - wg_first], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
-      }
-      if (in1) {
-        wg_dir[w][1] = ent1 >= 0 ? (int)(entry_offset(ent1)) : -1;
-        lold1 = __hip_atomic_fetch_add(&wg_cnt[f1.k0 - wg_first], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
-      }
+  // Note where each piece's record is, then count it (release: the
+  // directory entry and the record are visible before the count).
+  int lold0 = 0, lold1 = 0;
+  if (lane == 0) {
+    if (arr_s0 >= 0) {
+      wg_dir[w][0] = ent0 >= 0 ? entry_offset(ent0) : -1;
+      lold0 = __hip_atomic_fetch_add(&wg_cnt[p0.key], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
     }
-    const bool last0 = in0 && __shfl(lold0, 0) == f0.np - 1;
-    const bool last1 = in1 && __shfl(lold1, 0) == f1.np - 1;
-    if (last0 || last1) {
-      asm volatile("" ::: "memory");  // record reads are issued after this branch resolves
-      auto merge_local = [&](auto np_c, const SegInfo& f, int s, int g) __attribute__((always_inline)) {
-        constexpr int NP = decltype(np_c)::value;
-        const Pairs<NP> P = pairs_of<NP>(lane, G * 16);
-        Fold<NP> F;
-        fold_init(F);
-        fold_records(F, f.np, [&](int r, float(&m)[NP], float(&l)[NP], f32x4(&x0)[NP], f32x4(&x1)[NP])
-                                  __attribute__((always_inline)) {
-                                    const int slot = r == 0 ? f.first_slot : 2 * (f.k0 + r);
-                                    const int ow = __builtin_amdgcn_readfirstlane((slot >> 1) - wg_first);
-                                    const int d = __builtin_amdgcn_readfirstlane(wg_dir[ow][slot & 1]);
-                                    fetch_record(a, (size_t)slot, d >= 0 ? (const char*)stage_lds[ow] + d : nullptr,
-                                                 P, m, l, x0, x1);
-                                  });
-        write_rows(a, F, P, s, g);
-      };
-      for (int x = 0; x < 2; ++x) {
-        if (!(x == 0 ? last0 : last1)) continue;
-        const SegInfo f = x == 0 ? f0 : f1;
-        const int s = x == 0 ? arr_s0 : arr_s1, g = x == 0 ? arr_g0 : arr_g1;
-        if (G > 8) merge_local(std::integral_constant<int, 4>{}, f, s, g);
-        else merge_local(std::integral_constant<int, 2>{}, f, s, g);
-      }
+    if (arr_s1 >= 0) {
+      wg_dir[w][1] = ent1 >= 0 ? entry_offset(ent1) : -1;
+      lold1 = __hip_atomic_fetch_add(&wg_cnt[p1.key], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
     }
   }
-  if (!gl0 && !gl1) return;
+  const bool last0 = arr_s0 >= 0 && __shfl(lold0, 0) == p0.pkend - p0.pk0;
+  const bool last1 = arr_s1 >= 0 && __shfl(lold1, 0) == p1.pkend - p1.pk0;
+  if (!last0 && !last1) return;
+  asm volatile("" ::: "memory");  // record reads are issued after this branch resolves
+  // The workgroup's pieces that go on to stage 2 read their group counter
+  // now: the atomic's round trip overlaps the stage-1 fold.  A count showing
+  // every other workgroup piece of the group arrived cannot change.
+  int c0 = 0, c1 = 0;
+  if (lane == 0) {
+    if (last0 && p0.nwp > 1) c0 = __hip_atomic_load(group_cnt(p0.kg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (last1 && p1.nwp > 1) c1 = __hip_atomic_load(group_cnt(p1.kg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
 
-  // The last arrival of a group merges it.  One pass over the records covers
-  // every (head, 8-value chunk) pair of the GQA group: two pairs per lane up
-  // to 8 heads, four up to 16.
   // A counter is returned to zero by its last arrival, after this wave's
   // merges: no other wave touches it again in this launch, and a store ahead
   // of the record loads would make their wait include the store's
   // write-through (a wave's memory counter retires loads and stores in issue
   // order).  Bit x: group counter of piece x; bit 2 + x: its segment counter.
   unsigned rezero = 0;
-  auto merge_pieces = [&](auto np_c) __attribute__((always_inline)) {
+  auto merge = [&](auto np_c) __attribute__((always_inline)) {
     constexpr int NP = decltype(np_c)::value;
     const Pairs<NP> P = pairs_of<NP>(lane, G * 16);
     for (int x = 0; x < 2; ++x) {
-      const int s = x == 0 ? arr_s0 : arr_s1;
-      if (s < 0 || (x == 0 ? in0 : in1)) continue;
-      const int g = x == 0 ? arr_g0 : arr_g1;
-      const bool mine = x == 0 ? mine0 : mine1;
-      const char* const own_rec = x == 0 ? rec0 : rec1;
-      const SegInfo f = x == 0 ? f0 : f1;
-      auto piece_slot = [&](int r) __attribute__((always_inline)) {
-        return r == 0 ? (size_t)f.first_slot : (size_t)2 * (f.k0 + r);
+      if (!(x == 0 ? last0 : last1)) continue;
+      const Part p = x == 0 ? p0 : p1;
+      // stage 1: the workgroup's pieces of the segment, in order
+      Fold<NP> Fw;
+      fold_init(Fw);
+      fold_records(Fw, p.pkend - p.pk0 + 1, [&](int r, float(&m)[NP], float(&l)[NP], f32x4(&x0)[NP],
+                                                f32x4(&x1)[NP]) __attribute__((always_inline)) {
+        const int k = p.pk0 + r;
+        const int slot = k == p.k0 ? p.first_slot : 2 * k;
+        const int ow = __builtin_amdgcn_readfirstlane(k - wg_first);
+        const int d = __builtin_amdgcn_readfirstlane(wg_dir[ow][slot & 1]);
+        fetch_record(a, (size_t)slot, d >= 0 ? (const char*)stage_lds[ow] + d : nullptr, P, m, l, x0, x1);
+      });
+      if (p.nwp == 1) {  // the segment lies inside the workgroup
+        write_rows(a, Fw, P, p.s, p.g);
+        continue;
+      }
+      // stage 2: this workgroup's piece, as it would be stored
+      float wm[NP], wl[NP];
+      f32x4 wx0[NP], wx1[NP];
+      normalise(Fw, wm, wl, wx0, wx1);
+      auto wslot = [&](int r) __attribute__((always_inline)) {
+        return rec_wg + (r == 0 ? (size_t)p.first_wslot : (size_t)2 * (p.bk0 + r));
       };
-      if (!mine && __shfl(x == 0 ? old0 : old1, 0) != f.gn - 1) continue;  // not the group's last arrival
-      asm volatile("" ::: "memory");  // record loads are issued after this branch resolves
+      auto own_or = [&](bool own, size_t slot, const float(&om)[NP], const float(&ol)[NP], const f32x4(&ox0)[NP],
+                        const f32x4(&ox1)[NP], float(&m)[NP], float(&l)[NP], f32x4(&x0)[NP], f32x4(&x1)[NP])
+                        __attribute__((always_inline)) {
+        if (own) {
+#pragma unroll
+          for (int i = 0; i < NP; ++i) {
+            m[i] = om[i];
+            l[i] = ol[i];
+            x0[i] = ox0[i];
+            x1[i] = ox1[i];
+          }
+        } else {
+          fetch_record(a, slot, nullptr, P, m, l, x0, x1);
+        }
+      };
+      if (__shfl(x == 0 ? c0 : c1, 0) != p.gn - 1) {  // not yet the group's last arrival: publish and count
+        write_record(a, P, wslot(p.rb), wm, wl, wx0, wx1);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        int old = 0;
+        if (lane == 0) old = __hip_atomic_fetch_add(group_cnt(p.kg), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (__shfl(old, 0) != p.gn - 1) continue;
+        asm volatile("" ::: "memory");  // record loads are issued after this branch resolves
+      }
       rezero |= 1u << x;
-      // the group's pieces, in order (this wave's own piece from LDS)
-      const int own_idx = mine ? f.r - f.gfirst : -1;
+      // the group's workgroup pieces, in order (this workgroup's from registers)
+      const int own_u = p.rb - p.gfirst;
       Fold<NP> Fg;
       fold_init(Fg);
-      fold_records(Fg, f.gn, [&](int u, float(&m)[NP], float(&l)[NP], f32x4(&x0)[NP], f32x4(&x1)[NP])
+      fold_records(Fg, p.gn, [&](int u, float(&m)[NP], float(&l)[NP], f32x4(&x0)[NP], f32x4(&x1)[NP])
                                  __attribute__((always_inline)) {
-                                   fetch_record(a, u == own_idx ? 0 : piece_slot(f.gfirst + u),
-                                                u == own_idx ? own_rec : nullptr, P, m, l, x0, x1);
+                                   own_or(u == own_u, wslot(p.gfirst + u), wm, wl, wx0, wx1, m, l, x0, x1);
                                  });
-      if (f.ngroups == 1) {  // the group is the whole segment
-        write_rows(a, Fg, P, s, g);
+      if (p.ngroups == 1) {  // the group is the whole segment
+        write_rows(a, Fg, P, p.s, p.g);
         continue;
       }
       // Two levels.  This group's record, as it would be stored:
@@ -1013,7 +1014,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       f32x4 gx0[NP], gx1[NP];
       normalise(Fg, gm, gl, gx0, gx1);
       auto group_slot = [&](int c) __attribute__((always_inline)) {
-        return (size_t)2 * TW + f.k0 + min(f.np, (c + 1) * kFanIn) - 1;
+        return rec_grp + p.bk0 + min(p.nwp, (c + 1) * kFanIn) - 1;
       };
       // If every other group of the segment is merged by now (checked after
       // this group's fold, so that the others had that long to finish),
@@ -1021,55 +1022,35 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       // store, no second counter round trip.  Bit-identical to the path
       // through memory.
       int done = 0;
-      if (lane == 0) done = __hip_atomic_load(seg_cnt(f.kend), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const int c_own = f.gfirst / kFanIn;
-      if (__shfl(done, 0) == f.ngroups - 1) {
-        asm volatile("" ::: "memory");  // group record loads are issued after this branch resolves
-        rezero |= 4u << x;
-        Fold<NP> F;
-        fold_init(F);
-        fold_records(F, f.ngroups, [&](int u, float(&m)[NP], float(&l)[NP], f32x4(&x0)[NP], f32x4(&x1)[NP])
-                                       __attribute__((always_inline)) {
-                                         if (u == c_own) {
-#pragma unroll
-                                           for (int i = 0; i < NP; ++i) {
-                                             m[i] = gm[i];
-                                             l[i] = gl[i];
-                                             x0[i] = gx0[i];
-                                             x1[i] = gx1[i];
-                                           }
-                                         } else {
-                                           fetch_record(a, group_slot(u), nullptr, P, m, l, x0, x1);
-                                         }
-                                       });
-        write_rows(a, F, P, s, g);
-        continue;
+      if (lane == 0) done = __hip_atomic_load(seg_cnt(p.bkend), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int c_own = p.gfirst / kFanIn;
+      if (__shfl(done, 0) != p.ngroups - 1) {
+        write_record(a, P, rec_grp + p.kg, gm, gl, gx0, gx1);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        int old = 0;
+        if (lane == 0) old = __hip_atomic_fetch_add(seg_cnt(p.bkend), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (__shfl(old, 0) != p.ngroups - 1) continue;
       }
-      write_record(a, P, (size_t)2 * TW + f.kg, gm, gl, gx0, gx1);
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      int old = 0;
-      if (lane == 0) old = __hip_atomic_fetch_add(seg_cnt(f.kend), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (__shfl(old, 0) != f.ngroups - 1) continue;
-      asm volatile("" ::: "memory");
+      asm volatile("" ::: "memory");  // group record loads are issued after this branch resolves
       rezero |= 4u << x;
       Fold<NP> F;
       fold_init(F);
-      fold_records(F, f.ngroups, [&](int u, float(&m)[NP], float(&l)[NP], f32x4(&x0)[NP], f32x4(&x1)[NP])
+      fold_records(F, p.ngroups, [&](int u, float(&m)[NP], float(&l)[NP], f32x4(&x0)[NP], f32x4(&x1)[NP])
                                      __attribute__((always_inline)) {
-                                       fetch_record(a, group_slot(u), nullptr, P, m, l, x0, x1);
+                                       own_or(u == c_own, group_slot(u), gm, gl, gx0, gx1, m, l, x0, x1);
                                      });
-      write_rows(a, F, P, s, g);
+      write_rows(a, F, P, p.s, p.g);
     }
   };
   if (G > 8)
-    merge_pieces(std::integral_constant<int, 4>{});
+    merge(std::integral_constant<int, 4>{});
   else
-    merge_pieces(std::integral_constant<int, 2>{});
+    merge(std::integral_constant<int, 2>{});
   if (lane == 0) {
-    if (rezero & 1u) __hip_atomic_store(group_cnt(f0.kg), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (rezero & 2u) __hip_atomic_store(group_cnt(f1.kg), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (rezero & 4u) __hip_atomic_store(seg_cnt(f0.kend), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (rezero & 8u) __hip_atomic_store(seg_cnt(f1.kend), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (rezero & 1u) __hip_atomic_store(group_cnt(p0.kg), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (rezero & 2u) __hip_atomic_store(group_cnt(p1.kg), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (rezero & 4u) __hip_atomic_store(seg_cnt(p0.bkend), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (rezero & 8u) __hip_atomic_store(seg_cnt(p1.bkend), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -1192,7 +1173,7 @@ int validate(const dp_decode_shape* sh, Plan* plan) {
   // unit prefix, context lengths and fp8 scales (dynamic)
   const size_t stat = (size_t)kWaves * kMaxUnitsPerWave * (fp8 ? 4 : 2) * sizeof(int) + kWaves * sizeof(int) +
                       (size_t)kWaves * kStageBytes + (size_t)kWaves * kMaxStaged * (sizeof(long long) + sizeof(int)) +
-                      (size_t)kWaves * 3 * sizeof(int) + 256;
+                      (size_t)kWaves * 4 * sizeof(int) + 256;
   plan->dyn_lds = (size_t)(2 * sh->batch + 1 + 2 * sh->n_kv_heads) * 4;
   if (stat + plan->dyn_lds > kLdsBytes)
     return fail(DP_ENOTSUP, "paged_decode: %zu bytes of LDS per workgroup", stat + plan->dyn_lds);

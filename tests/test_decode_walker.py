@@ -33,7 +33,7 @@ import pytest
 
 WAVES = 4               # waves per workgroup
 MAX_UNITS_PER_WAVE = 256
-FAN_IN = 8              # pieces per merge group
+FAN_IN = 16             # workgroup pieces per merge group
 
 
 def host_plan(ctx, hkv, fp8, max_ctx, partition_tokens=0, wgs_per_cu=0, cus=256, resident=2):
@@ -192,7 +192,9 @@ def check(sim, hkv):
     for s, blk, nb in sim["bt_reads"]:
         assert 0 <= blk < nb <= sim["max_blocks_per_seq"], (s, blk, nb)
     assert sorted(sim["computed"]) == list(range(sim["U"]))
-    counters_group, counters_seg = set(), set()
+    counters_group, counters_seg, shares = set(), set(), set()
+    nwg = TW // WAVES
+    CW = WAVES * C
     for (s, g), got in sim["pieces"].items():
         nus = pre[s + 1] - pre[s]
         a0 = hkv * pre[s] + g * nus
@@ -204,14 +206,27 @@ def check(sim, hkv):
         assert sorted(by_wave) == list(range(k0, kend + 1))
         for r in range(np_):
             assert by_wave[k0 + r] == (first_slot if r == 0 else 2 * (k0 + r))
-        for gfirst in range(0, np_, FAN_IN):
-            gn = min(np_, gfirst + FAN_IN) - gfirst
-            kg = k0 + gfirst + gn - 1
-            assert 0 <= kg < TW and 2 * TW + kg < 3 * TW
+        # stage 1: one LDS counter per share of a workgroup, keyed by its first piece
+        for b in range(k0 // WAVES, kend // WAVES + 1):
+            pk0 = max(k0, b * WAVES)
+            key = 2 * (pk0 - b * WAVES) + ((first_slot & 1) if pk0 == k0 else 0)
+            assert 0 <= key < 2 * WAVES and (b, key) not in shares
+            shares.add((b, key))
+        # stage 2: workgroup pieces, groups of FAN_IN, device-wide counters per workgroup
+        bk0, bkend = a0 // CW, (a0 + nus - 1) // CW
+        nwp = bkend - bk0 + 1
+        if nwp == 1:
+            continue
+        first_wslot = 2 * bk0 + (1 if a0 > bk0 * CW else 0)
+        assert 2 * TW + first_wslot < 2 * TW + 2 * nwg and 2 * TW + 2 * bkend < 2 * TW + 2 * nwg
+        for gfirst in range(0, nwp, FAN_IN):
+            gn = min(nwp, gfirst + FAN_IN) - gfirst
+            kg = bk0 + gfirst + gn - 1
+            assert 0 <= kg < nwg and 2 * TW + 2 * nwg + kg < 3 * TW
             assert kg not in counters_group
             counters_group.add(kg)
-        assert 0 <= kend < TW and kend not in counters_seg
-        counters_seg.add(kend)
+        assert 0 <= bkend < nwg and bkend not in counters_seg
+        counters_seg.add(bkend)
     for slot in sim["records"]:
         assert 0 <= slot < 2 * TW
 
@@ -269,125 +284,109 @@ def test_benchmark_shapes():
 
 # ---------------------------------------------------------------- end-of-slice merge protocol
 
-def run_merge_protocol(sim, rng, p_staged=0.8):
+def run_merge_protocol(sim, rng):
     """Play the kernel's end-of-slice protocol for every split piece, with the
     waves' steps interleaved in a random order, and check that every cut
     segment is written exactly once, that no merge reads a record before it
     is published, and that every counter is zero afterwards.
 
-    Per wave, as the kernel orders it: read both group counters (atomic
-    loads) for pieces whose record is still staged in LDS; publish and count
-    the pieces that were not found to be the group's last; count the pieces
-    of segments that lie inside one workgroup on that workgroup's counter
-    (their last arrival writes the segment, and they touch no global
-    counter); then, piece by
-    piece, the group's last arrival merges the group and either writes the
-    segment or goes through the segment counter (load, then group record and
-    increment unless every other group is done); last, after a step of its
-    own, the wave returns to zero every counter it was the last arrival of.
-    No wave may read or count a counter between its last arrival and that
-    reset."""
-    C, pre = sim["C"], sim["pre"]
-    hkv = sim["hkv"]
-    seg_of_piece = {}
+    Per wave, as the kernel orders it.  Stage 1: for each split piece, note
+    where its record is (its LDS staging area, or its wave slot when a
+    mid-loop flush wrote it, which then has completed) and count it on the
+    LDS counter of the segment's share of the workgroup; the share's last
+    arrival folds the share's pieces.  A segment inside the workgroup is then
+    written.  Stage 2, for a share of a segment that crosses workgroups: read
+    the group counter (an atomic load, issued before the stage-1 fold); unless
+    it shows every other workgroup piece of the group arrived, publish the
+    workgroup piece and count it; the group's last arrival folds the group and
+    either writes the segment or goes through the segment counter (load, then
+    group record and increment unless every other group is done).  Last,
+    after a step of its own, the wave returns to zero every device-wide
+    counter it was the last arrival of.  No wave may read or count a counter
+    between its last arrival and that reset."""
+    C, pre, hkv, TW = sim["C"], sim["pre"], sim["hkv"], sim["TW"]
+    CW = WAVES * C
     waves = {}
     for (s, g), got in sim["pieces"].items():
         nus = pre[s + 1] - pre[s]
         a0 = hkv * pre[s] + g * nus
         k0, kend = a0 // C, (a0 + nus - 1) // C
-        np_ = kend - k0 + 1
-        for r in range(np_):
-            gfirst = r - r % FAN_IN
-            gn = min(np_, gfirst + FAN_IN) - gfirst
-            info = dict(seg=(s, g), r=r, gfirst=gfirst, gn=gn, kg=k0 + gfirst + gn - 1, ngroups=-(-np_ // FAN_IN),
-                        kend=kend, np=np_, k0=k0, local=k0 // WAVES == kend // WAVES)
-            w = k0 + r
-            seg_of_piece[(w, r == 0)] = info
-            waves.setdefault(w, []).append(info)
-    group_cnt, seg_cnt, wg_cnt = {}, {}, {}
-    published, group_published, written = set(), set(), {}
-    published_local = set()  # pieces of segments merged inside their workgroup
+        first_slot = 2 * k0 + (1 if a0 > k0 * C else 0)
+        bk0, bkend = a0 // CW, (a0 + nus - 1) // CW
+        nwp = bkend - bk0 + 1
+        for k in range(k0, kend + 1):
+            b = k // WAVES
+            pk0, pkend = max(k0, b * WAVES), min(kend, b * WAVES + WAVES - 1)
+            rb = b - bk0
+            gfirst = rb - rb % FAN_IN
+            gn = min(nwp, gfirst + FAN_IN) - gfirst
+            waves.setdefault(k, []).append(dict(
+                seg=(s, g), k=k, share=(b, 2 * (pk0 - b * WAVES) + ((first_slot & 1) if pk0 == k0 else 0)),
+                share_waves=list(range(pk0, pkend + 1)), nwp=nwp, rb=rb, gfirst=gfirst, gn=gn,
+                kg=bk0 + gfirst + gn - 1, ngroups=-(-nwp // FAN_IN), bkend=bkend))
+    wg_cnt, group_cnt, seg_cnt = {}, {}, {}
+    published_local, wg_published, group_published, written = set(), set(), set(), {}
     done_group, done_seg = set(), set()  # counters whose last arrival has come, not yet reset
 
     def read(cnt, done, k):
         assert k not in done, f"counter {k} read after its last arrival"
         return cnt.get(k, 0)
 
-    def merge_group(info, own):
-        seg = info["seg"]
-        for u in range(info["gn"]):
-            r = info["gfirst"] + u
-            if not (own and r == info["r"]):
-                assert (seg, r) in published, f"merge of {seg} read piece {r} before it was published"
-        done_group.add(info["kg"])
-
     def steps_of(w):
-        pieces = sorted(waves[w], key=lambda i: i["r"] != 0)  # the slice's first piece, then its last
-        staged = [bool(rng.random() < p_staged) for _ in pieces]
-        mine = [False] * len(pieces)
-        # 1. atomic loads of the group counters (records still in LDS); pieces
-        # of segments inside one workgroup take no part in the global protocol
-        for x, info in enumerate(pieces):
-            if staged[x] and not info["local"]:
-                mine[x] = read(group_cnt, done_group, info["kg"]) == info["gn"] - 1
+        pieces = waves[w]
+        # stage 1: publish and count every piece on its share's LDS counter
+        lasts = []
+        for info in pieces:
+            published_local.add((info["seg"], info["k"]))
+            old = wg_cnt.get(info["share"], 0)
+            wg_cnt[info["share"]] = old + 1
+            if old == len(info["share_waves"]) - 1:
+                lasts.append(info)
+            yield
+        if not lasts:
+            return
+        # group counters of the shares going on to stage 2 are read before the folds
+        early = [read(group_cnt, done_group, info["kg"]) if info["nwp"] > 1 else None for info in lasts]
         yield
-        # 2. publish and count the others
-        last = [False] * len(pieces)
-        for x, info in enumerate(pieces):
-            if not mine[x] and not info["local"]:
-                published.add((info["seg"], info["r"]))
+        resets = []
+        for info, c in zip(lasts, early):
+            seg = info["seg"]
+            for k in info["share_waves"]:
+                assert (seg, k) in published_local, f"share of {seg} read piece of wave {k} before it was published"
+            if info["nwp"] == 1:
+                written[seg] = written.get(seg, 0) + 1
+                continue
+            if c != info["gn"] - 1:
+                wg_published.add((seg, info["rb"]))
                 old = read(group_cnt, done_group, info["kg"])
                 group_cnt[info["kg"]] = old + 1
-                last[x] = old == info["gn"] - 1
                 yield
-        # 2b. segments inside the workgroup: publish the record's place, count
-        # on the workgroup's counter (keyed by the segment's first wave); the
-        # last arrival folds every piece and writes the segment
-        for x, info in enumerate(pieces):
-            if not info["local"]:
-                continue
-            seg = info["seg"]
-            published_local.add((seg, info["r"]))
-            key = (info["k0"] // WAVES, info["k0"])
-            old = wg_cnt.get(key, 0)
-            wg_cnt[key] = old + 1
-            if old == info["np"] - 1:
-                for r in range(info["np"]):
-                    assert (seg, r) in published_local, f"local merge of {seg} read piece {r} before it was published"
-                written[seg] = written.get(seg, 0) + 1
-            yield
-        # 3. merges
-        resets = []
-        for x, info in enumerate(pieces):
-            if info["local"] or not (mine[x] or last[x]):
-                continue
-            merge_group(info, mine[x])
+                if old != info["gn"] - 1:
+                    continue
+            for u in range(info["gn"]):
+                rb = info["gfirst"] + u
+                if rb != info["rb"]:
+                    assert (seg, rb) in wg_published, f"group of {seg} read workgroup piece {rb} before it was published"
+            done_group.add(info["kg"])
             resets.append((group_cnt, done_group, info["kg"]))
-            yield
-            seg = info["seg"]
             if info["ngroups"] == 1:
                 written[seg] = written.get(seg, 0) + 1
                 continue
             c_own = info["gfirst"] // FAN_IN
-            if read(seg_cnt, done_seg, info["kend"]) == info["ngroups"] - 1:
-                for c in range(info["ngroups"]):
-                    if c != c_own:
-                        assert (seg, c) in group_published, f"{seg}: group {c} read before it was published"
-                done_seg.add(info["kend"])
-                resets.append((seg_cnt, done_seg, info["kend"]))
-                written[seg] = written.get(seg, 0) + 1
-                continue
-            group_published.add((seg, c_own))
-            old = read(seg_cnt, done_seg, info["kend"])
-            seg_cnt[info["kend"]] = old + 1
-            yield
-            if old == info["ngroups"] - 1:
-                for c in range(info["ngroups"]):
-                    assert (seg, c) in group_published
-                done_seg.add(info["kend"])
-                resets.append((seg_cnt, done_seg, info["kend"]))
-                written[seg] = written.get(seg, 0) + 1
-        # 4. the counters this wave was the last arrival of return to zero
+            if read(seg_cnt, done_seg, info["bkend"]) != info["ngroups"] - 1:
+                group_published.add((seg, c_own))
+                old = read(seg_cnt, done_seg, info["bkend"])
+                seg_cnt[info["bkend"]] = old + 1
+                yield
+                if old != info["ngroups"] - 1:
+                    continue
+            for c in range(info["ngroups"]):
+                if c != c_own:
+                    assert (seg, c) in group_published, f"{seg}: group {c} read before it was published"
+            done_seg.add(info["bkend"])
+            resets.append((seg_cnt, done_seg, info["bkend"]))
+            written[seg] = written.get(seg, 0) + 1
+        # the device-wide counters this wave was the last arrival of return to zero
         yield
         for cnt, done, k in resets:
             cnt[k] = 0
@@ -403,10 +402,12 @@ def run_merge_protocol(sim, rng, p_staged=0.8):
     assert written == {seg: 1 for seg in sim["pieces"]}, "a cut segment was written other than once"
     assert all(v == 0 for v in group_cnt.values()) and all(v == 0 for v in seg_cnt.values())
     assert not done_group and not done_seg
-    # every local counter saw exactly its segment's pieces (no reset needed:
-    # the counters live in LDS for one launch)
-    for (wg, k0), v in wg_cnt.items():
-        assert v == next(i["np"] for ws in waves.values() for i in ws if i["k0"] == k0 and i["local"])
+    # every share's LDS counter saw exactly the share's pieces (no reset: LDS lives one launch)
+    shares = {}
+    for ws in waves.values():
+        for info in ws:
+            shares[info["share"]] = len(info["share_waves"])
+    assert wg_cnt == shares
 
 
 @pytest.mark.parametrize("fp8", [False, True])
@@ -441,16 +442,31 @@ def test_largest_batch_reaches_both_local_merge_sources(fp8):
 
 @pytest.mark.parametrize("trial", range(30))
 def test_merge_protocol_any_arrival_order(trial):
-    """Random batches (including long segments cut into more than eight pieces,
-    which merge on two levels) under random interleavings of the waves' steps."""
+    """Random batches (segments inside one workgroup, across a few, and across
+    more than sixteen, which merge on two levels) under random interleavings
+    of the waves' steps."""
     rng = np.random.default_rng(7000 + trial)
     fp8 = bool(trial % 2)
     B = int(rng.choice([2, 5, 16, 40]))
     hkv = int(rng.choice([1, 2, 4]))
     max_ctx = int(rng.choice([300, 3000, 20000]))
     ctx = draw(rng, B, max_ctx, 0.2)
-    cus = int(rng.choice([2, 8, 32]))
+    cus = int(rng.choice([2, 8, 32, 96]))
     sim = simulate(ctx, hkv, fp8, max_ctx, -(-max_ctx // 16), 0, 0, cus)
     sim["hkv"] = hkv
     for rep in range(3):
-        run_merge_protocol(sim, np.random.default_rng(rep + 10 * trial), p_staged=float(rng.choice([0.0, 0.5, 1.0])))
+        run_merge_protocol(sim, np.random.default_rng(rep + 10 * trial))
+
+
+@pytest.mark.parametrize("trial", range(6))
+def test_merge_protocol_two_levels(trial):
+    """One long sequence cut across 64 workgroups (groups of sixteen workgroup
+    pieces, then the groups) beside short ones, under random interleavings."""
+    rng = np.random.default_rng(7100 + trial)
+    ctx = [60000] + list(rng.integers(1, 3000, 7))
+    sim = simulate(ctx, 1, bool(trial % 2), 60000, 3750, 0, 0, 64)
+    sim["hkv"] = 1
+    C, pre = sim["C"], sim["pre"]
+    assert -(-(pre[1] - pre[0]) // (WAVES * C)) > FAN_IN  # the long segment spans more than one group
+    for rep in range(3):
+        run_merge_protocol(sim, np.random.default_rng(rep + 10 * trial))
