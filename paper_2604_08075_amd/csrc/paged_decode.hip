@@ -76,6 +76,7 @@ constexpr int kMaxUnitsPerWave = 256;  // the host sizes the grid so that no sli
 // after the loop (global stores share the in-order memory counter with the
 // KV loads; a store issued inside the loop would make the next wait cover it).
 constexpr int kStageBytes = 24 * 1024;  // per wave
+constexpr int kRecBytes = 8192 + 512;  // a staged record: eight 1 KiB chunks of o, then (m, l) per lane
 constexpr int kMaxStaged = 6;           // entries per wave
 
 struct DecodeArgs {
@@ -206,17 +207,15 @@ __device__ __forceinline__ void store_out8(const DecodeArgs& a, size_t off, f32x
   }
 }
 
-// Records (o, m, l): o normalised by l, m in log2 units.  Slots 2k and
-// 2k + 1 hold the first and last split piece of wave k when a staging area
-// that fills up in the middle of a slice writes them out.  A segment cut by
-// slice boundaries is merged in two stages: first inside each workgroup
-// (through LDS), then across workgroups.  Slots 2 * waves + 2b and
-// 2 * waves + 2b + 1 hold workgroup b's first and last piece of segments that
-// cross its edges, and 2 * waves + 2 * workgroups + b the merged record of
-// the group of workgroup pieces whose last is workgroup b's.  Workgroup
-// pieces are merged in groups of kFanIn consecutive ones, then the group
-// records, so that a segment cut into many pieces needs few memory round
-// trips on each level.
+// Records (o, m, l): o normalised by l, m in log2 units.  A segment cut by
+// slice boundaries is merged in two stages: first inside each workgroup,
+// from the records its waves keep in their LDS staging areas, then across
+// workgroups through the workspace.  Slots 2b and 2b + 1 hold workgroup b's
+// first and last piece of segments that cross its edges, and
+// 2 * workgroups + b the merged record of the group of workgroup pieces
+// whose last is workgroup b's.  Workgroup pieces are merged in groups of
+// kFanIn consecutive ones, then the group records, so that a segment cut
+// into many pieces needs few memory round trips on each level.
 constexpr int kFanIn = 16;
 
 // Log-sum-exp fold of records, by one wave, in record order:
@@ -399,7 +398,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   // Split pieces are first merged inside the workgroup: arrivals per share
   // of a segment (keyed by the share's first piece: wave, first or last), and
   // where each wave's split pieces' records are (byte offset in its staging
-  // area, or -1: in their wave slot).
+  // area).
   __shared__ int wg_cnt[2 * kWaves];
   __shared__ int wg_dir[kWaves][2];
   __shared__ __attribute__((aligned(16))) char stage_lds[kWaves][kStageBytes];
@@ -582,46 +581,42 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   char* const stg = stage_lds[w];
   int st_n = 0, st_off = 0;  // entries and bytes staged (wave-uniform)
   int first_entry = -1;      // staging entry of the slice's first piece record while it is still staged
-  // pass 0 writes every entry and empties the staging area; pass 1 writes
-  // only the records (the entries in `skip`, a bit mask, excepted), pass 2
-  // only the rows, and empties it.
-  auto flush = [&](unsigned skip, int pass) __attribute__((always_inline)) {
-    if (pass == 0) first_entry = -1;  // the first piece's record is written out
+  // Write the staged rows out and empty the staging list.  Records are never
+  // written: a wave stages at most two, the first of them is always the first
+  // entry and is kept (below), and the second is staged last.
+  auto flush = [&]() __attribute__((always_inline)) {
     for (int e = 0; e < st_n; ++e) {
-      if ((skip >> e) & 1u) continue;
       const int ko = __builtin_amdgcn_readfirstlane(stage_kind[w][e]);
       const int kind = ko & 15;
-      if ((pass == 1 && kind != 2) || (pass == 2 && kind == 2)) continue;
+      if (kind == 2) continue;
       const char* base = stg + (ko >> 4);
       const long long dst = stage_dst[w][e];
       const unsigned dlo = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)(dst & 0xffffffffll));
       const unsigned dhi = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)((unsigned long long)dst >> 32));
       const size_t d = ((size_t)dhi << 32) | dlo;
       if (li >= G) continue;
-      if (kind == 2) {  // partial record, slot d
-        const __amdgpu_buffer_rsrc_t r = record_rsrc(a.rec_o, d, G);
-        for (int nn = 0; nn < 8; ++nn)
-          coherent_store16(r, (li * kHeadDim + 16 * nn + 4 * lj) * 4, *(const f32x4*)(base + nn * 1024 + lane * 16));
-        if (lj == 0) {
-          const float* ml = (const float*)(base + 8192 + lane * 8);
-          coherent_store2(a.rec_ml + (d * G + li) * 2, ml[0], ml[1]);
-        }
-      } else {  // output rows of one (sequence, KV head): d is the element offset of its first row
-        const size_t row = d + (size_t)li * kHeadDim;
-        for (int nn = 0; nn < 8; ++nn) {
-          const size_t off = row + 16 * nn + 4 * lj;
-          if (kind == 1) *(f32x4*)((float*)a.out + off) = *(const f32x4*)(base + nn * 1024 + lane * 16);
-          else *(u16x4*)((uint16_t*)a.out + off) = *(const u16x4*)(base + nn * 512 + lane * 8);
-        }
+      // output rows of one (sequence, KV head): d is the element offset of its first row
+      const size_t row = d + (size_t)li * kHeadDim;
+      for (int nn = 0; nn < 8; ++nn) {
+        const size_t off = row + 16 * nn + 4 * lj;
+        if (kind == 1) *(f32x4*)((float*)a.out + off) = *(const f32x4*)(base + nn * 1024 + lane * 16);
+        else *(u16x4*)((uint16_t*)a.out + off) = *(const u16x4*)(base + nn * 512 + lane * 8);
       }
     }
-    if (pass != 1) {
-      st_n = 0;
-      st_off = 0;
-    }
+    st_n = 0;
+    st_off = 0;
   };
   auto stage_begin = [&](int bytes) __attribute__((always_inline)) {  // room for one entry; returns its LDS offset
-    if (st_n == kMaxStaged || st_off + bytes > kStageBytes) flush(0u, 0);
+    if (st_n == kMaxStaged || st_off + bytes > kStageBytes) {
+      // Write the rows out.  The record of the slice's first piece, when it
+      // has one, is always the first entry, at offset 0: it stays for the
+      // merge.  Two records fit together.
+      flush();
+      if (first_entry == 0) {
+        st_n = 1;
+        st_off = kRecBytes;
+      }
+    }
     const int off = st_off;
     st_off += bytes;
     return off;
@@ -773,7 +768,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       }
       stage_meta(a.out_fp32 ? 1 : 0, (int)(base - stg), ((long long)cs.s * a.hq + (long long)cs.g * G) * kHeadDim);
     } else {  // a piece of a segment cut by slice boundaries
-      char* base = stg + stage_begin(8192 + 512);
+      char* base = stg + stage_begin(kRecBytes);
 #pragma unroll
       for (int nn = 0; nn < 8; ++nn) *(f32x4*)(base + nn * 1024 + lane * 16) = acc[nn] * inv;
       float* ml = (float*)(base + 8192 + lane * 8);
@@ -851,9 +846,8 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   // ---- 5. merge the split pieces ----
   // Stage 1, inside the workgroup: each piece of a segment is counted on an
   // LDS counter of the segment's share of this workgroup (keyed by the share's
-  // first piece), after its owner has noted where its record is: in its LDS
-  // staging area, or in its wave slot when a mid-loop flush wrote it out.  The
-  // last arrival folds the share's pieces in order.  A segment entirely inside
+  // first piece), after its owner has noted where in its LDS staging area the
+  // piece's record is.  The last arrival folds the share's pieces in order.  A segment entirely inside
   // the workgroup is then written; the share of a segment that crosses the
   // workgroup's edges is the workgroup's piece for stage 2.
   // Stage 2, across workgroups: workgroup pieces are merged in groups of
@@ -868,7 +862,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   const int wg_first = gw - w;          // first wave of this workgroup
   const int nwg = (int)gridDim.x;
   const int CW = kWaves * C;            // units per workgroup
-  const size_t rec_wg = (size_t)2 * TW;                // workgroup piece slots
+  const size_t rec_wg = 0;                             // workgroup piece slots
   const size_t rec_grp = rec_wg + (size_t)2 * nwg;     // group record slots
   struct Part {
     int s, g, k0, first_slot, pk0, pkend, key;         // the segment's waves; this workgroup's share of them
@@ -905,24 +899,22 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   Part p0 = {}, p1 = {};
   if (arr_s0 >= 0) p0 = part_of(arr_s0, arr_g0);
   if (arr_s1 >= 0) p1 = part_of(arr_s1, arr_g1);
-  // A record written out by a mid-loop flush has reached the coherence point
-  // before its piece is counted.
-  if ((arr_s0 >= 0 && ent0 < 0) || (arr_s1 >= 0 && ent1 < 0)) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  flush(0u, 2);  // finished rows; the pieces' records stay in the staging area
+  flush();  // finished rows; the pieces' records stay in the staging area
   if (arr_s0 < 0 && arr_s1 < 0) return;
   auto entry_offset = [&](int e) __attribute__((always_inline)) {
     return __builtin_amdgcn_readfirstlane(stage_kind[w][e]) >> 4;  // byte offset of entry e in the staging area
   };
-  // Note where each piece's record is, then count it (release: the
-  // directory entry and the record are visible before the count).
+  // Note where each piece's record is in the staging area, then count it
+  // (release: the directory entry and the record are visible before the
+  // count).
   int lold0 = 0, lold1 = 0;
   if (lane == 0) {
     if (arr_s0 >= 0) {
-      wg_dir[w][0] = ent0 >= 0 ? entry_offset(ent0) : -1;
+      wg_dir[w][0] = entry_offset(ent0);
       lold0 = __hip_atomic_fetch_add(&wg_cnt[p0.key], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
     }
     if (arr_s1 >= 0) {
-      wg_dir[w][1] = ent1 >= 0 ? entry_offset(ent1) : -1;
+      wg_dir[w][1] = entry_offset(ent1);
       lold1 = __hip_atomic_fetch_add(&wg_cnt[p1.key], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
     }
   }
@@ -957,10 +949,10 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       fold_records(Fw, p.pkend - p.pk0 + 1, [&](int r, float(&m)[NP], float(&l)[NP], f32x4(&x0)[NP],
                                                 f32x4(&x1)[NP]) __attribute__((always_inline)) {
         const int k = p.pk0 + r;
-        const int slot = k == p.k0 ? p.first_slot : 2 * k;
+        const int x = k == p.k0 ? (p.first_slot & 1) : 0;  // the wave's first or last piece
         const int ow = __builtin_amdgcn_readfirstlane(k - wg_first);
-        const int d = __builtin_amdgcn_readfirstlane(wg_dir[ow][slot & 1]);
-        fetch_record(a, (size_t)slot, d >= 0 ? (const char*)stage_lds[ow] + d : nullptr, P, m, l, x0, x1);
+        const int d = __builtin_amdgcn_readfirstlane(wg_dir[ow][x]);
+        fetch_record(a, 0, (const char*)stage_lds[ow] + d, P, m, l, x0, x1);
       });
       if (p.nwp == 1) {  // the segment lies inside the workgroup
         write_rows(a, Fw, P, p.s, p.g);
@@ -1202,8 +1194,9 @@ int validate(const dp_decode_shape* sh, Plan* plan) {
   plan->clear_words = waves > cap_waves ? (int)(2 * waves) : 0;
   plan->arrivals_off = 0;
   plan->rec_ml_off = align256(2 * counter_waves * sizeof(int32_t));
-  plan->rec_o_off = plan->rec_ml_off + align256(3 * waves * G * 2 * sizeof(float));
-  plan->ws_bytes = plan->rec_o_off + align256(3 * waves * G * kHeadDim * sizeof(float));
+  // records: two workgroup pieces and one group record per workgroup
+  plan->rec_o_off = plan->rec_ml_off + align256(3 * (size_t)grid * G * 2 * sizeof(float));
+  plan->ws_bytes = plan->rec_o_off + align256(3 * (size_t)grid * G * kHeadDim * sizeof(float));
   return DP_OK;
 }
 

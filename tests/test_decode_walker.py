@@ -172,14 +172,18 @@ ROW_BYTES, REC_BYTES = 4096, 8192 + 512     # one (sequence, KV head)'s bf16 row
 
 
 def flushed_mid_loop(entries, row_bytes=ROW_BYTES):
-    """Record slots a wave's staging writes out before its slice ends: the
-    kernel flushes every staged entry when the next one would not fit."""
+    """Record slots a wave's staging would write out before its slice ends.
+    When the next entry does not fit, the kernel writes the staged rows out
+    and keeps the first entry if it is a record (the slice's first piece);
+    the staging must never have to drop a record."""
     out, st_n, st_off, pending = set(), 0, 0, []
     for kind, slot in entries:
         size = row_bytes if kind == "row" else REC_BYTES
         if st_n == MAX_STAGED or st_off + size > STAGE_BYTES:
-            out |= {x for x in pending if x is not None}
-            st_n, st_off, pending = 0, 0, []
+            keep = pending[:1] if pending and pending[0] is not None else []
+            out |= {x for x in pending[len(keep):] if x is not None}
+            st_n, st_off, pending = len(keep), REC_BYTES * len(keep), keep
+        assert st_off + size <= STAGE_BYTES and st_n < MAX_STAGED
         st_n, st_off = st_n + 1, st_off + size
         pending.append(slot)
     return out
@@ -411,33 +415,26 @@ def run_merge_protocol(sim, rng):
 
 
 @pytest.mark.parametrize("fp8", [False, True])
-def test_largest_batch_reaches_both_local_merge_sources(fp8):
-    """The GPU test of the largest batch (4,096 short contexts, 2 KV heads)
-    merges segments cut inside one workgroup from both places a piece's record
-    can be: still in its owner's LDS staging area, and in its global slot after
-    a mid-loop flush.  Replays that batch's slices and staging here."""
+@pytest.mark.parametrize("row_bytes", [ROW_BYTES, 2 * ROW_BYTES])
+def test_records_stay_in_lds(fp8, row_bytes):
+    """A wave's split-piece records are never written out by its staging: the
+    merge reads every one from its owner's LDS.  Checked on the largest-batch
+    GPU case (4,096 short contexts: many rows per slice) and random batches,
+    with bf16 and fp32 rows."""
     rng = np.random.default_rng(31)
     ctx = rng.integers(0, 97, 4096)
     ctx[rng.integers(0, 4096, 64)] = 0
-    sim = simulate(list(ctx), 2, fp8, int(ctx.max()), 8)  # the workload's max_context_len and table width
-    check(sim, 2)
-    flushed = set()
-    for entries in sim["staged"].values():
-        flushed |= flushed_mid_loop(entries)
-    C, pre = sim["C"], sim["pre"]
-    in_lds = in_slot = 0
-    for (s_, g), got in sim["pieces"].items():
-        nus = pre[s_ + 1] - pre[s_]
-        a0 = 2 * pre[s_] + g * nus
-        k0, kend = a0 // C, (a0 + nus - 1) // C
-        if k0 // WAVES != kend // WAVES:
-            continue
-        for _, slot in got:
-            if slot in flushed:
-                in_slot += 1
-            else:
-                in_lds += 1
-    assert in_lds > 0 and in_slot > 0, (in_lds, in_slot)
+    cases = [(list(ctx), 2, int(ctx.max()), 8)]
+    for trial in range(20):
+        r = np.random.default_rng(500 + trial)
+        B = int(r.choice([3, 40, 300, 2000]))
+        max_ctx = int(r.choice([50, 300, 3000]))
+        cases.append((list(draw(r, B, max_ctx, 0.2)), int(r.choice([1, 2, 8])), max_ctx, -(-max_ctx // 16)))
+    for c, hkv, max_ctx, mbps in cases:
+        sim = simulate(c, hkv, fp8, max_ctx, mbps)
+        check(sim, hkv)
+        for entries in sim["staged"].values():
+            assert flushed_mid_loop(entries, row_bytes) == set()
 
 
 @pytest.mark.parametrize("trial", range(30))
