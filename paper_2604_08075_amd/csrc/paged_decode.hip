@@ -75,9 +75,7 @@ constexpr int kMaxUnitsPerWave = 256;  // the host sizes the grid so that no sli
 // Finished output rows and partial records are staged in LDS and written out
 // after the loop (global stores share the in-order memory counter with the
 // KV loads; a store issued inside the loop would make the next wait cover it).
-constexpr int kStageBytes = 24 * 1024;  // per wave
 constexpr int kRecBytes = 8192 + 512;  // a staged record: eight 1 KiB chunks of o, then (m, l) per lane
-constexpr int kMaxStaged = 6;           // entries per wave
 
 struct DecodeArgs {
   const uint16_t* q;            // [B, Hq, 128] bf16
@@ -396,14 +394,9 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   __shared__ int tiles_lds[kWaves][kMaxUnitsPerWave * UB];
   __shared__ int wave_sums[kWaves];
   // Split pieces are first merged inside the workgroup: arrivals per share
-  // of a segment (keyed by the share's first piece: wave, first or last), and
-  // where each wave's split pieces' records are (byte offset in its staging
-  // area).
+  // of a segment, keyed by the share's first piece (wave, first or last).
   __shared__ int wg_cnt[2 * kWaves];
-  __shared__ int wg_dir[kWaves][2];
-  __shared__ __attribute__((aligned(16))) char stage_lds[kWaves][kStageBytes];
-  __shared__ long long stage_dst[kWaves][kMaxStaged];  // element offset of a row in `out`, or a record slot
-  __shared__ int stage_kind[kWaves][kMaxStaged];       // 0 bf16 row, 1 fp32 row, 2 record
+  __shared__ __attribute__((aligned(16))) char stage_lds[kWaves][2 * kRecBytes];  // each wave's two records
   extern __shared__ int dyn[];  // pre[B + 1], ctxs[B], k_scale[Hkv], v_scale[Hkv]
 
   const int lane = threadIdx.x & 63;
@@ -575,59 +568,11 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     for (int x = 0; x < 8; ++x) R.v[x] = __builtin_nontemporal_load((const i32x4*)(vb + vofs[x]));
   };
 
-  // ---- staging of finished rows and records in LDS ----
-  // Entry layout: eight 16-byte (fp32) or 8-byte (bf16) chunks per lane,
-  // chunk-major ([nn][lane]), then for a record each lane's (m, l).
+  // ---- the records of this wave's split pieces, in LDS ----
+  // At most two: the slice's first piece (x = 0) at offset 0, its last
+  // (x = 1) at kRecBytes.  Layout: eight 1 KiB chunks of o ([nn][lane], 16
+  // bytes per lane), then each lane's (m, l).  They stay there for the merge.
   char* const stg = stage_lds[w];
-  int st_n = 0, st_off = 0;  // entries and bytes staged (wave-uniform)
-  int first_entry = -1;      // staging entry of the slice's first piece record while it is still staged
-  // Write the staged rows out and empty the staging list.  Records are never
-  // written: a wave stages at most two, the first of them is always the first
-  // entry and is kept (below), and the second is staged last.
-  auto flush = [&]() __attribute__((always_inline)) {
-    for (int e = 0; e < st_n; ++e) {
-      const int ko = __builtin_amdgcn_readfirstlane(stage_kind[w][e]);
-      const int kind = ko & 15;
-      if (kind == 2) continue;
-      const char* base = stg + (ko >> 4);
-      const long long dst = stage_dst[w][e];
-      const unsigned dlo = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)(dst & 0xffffffffll));
-      const unsigned dhi = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)((unsigned long long)dst >> 32));
-      const size_t d = ((size_t)dhi << 32) | dlo;
-      if (li >= G) continue;
-      // output rows of one (sequence, KV head): d is the element offset of its first row
-      const size_t row = d + (size_t)li * kHeadDim;
-      for (int nn = 0; nn < 8; ++nn) {
-        const size_t off = row + 16 * nn + 4 * lj;
-        if (kind == 1) *(f32x4*)((float*)a.out + off) = *(const f32x4*)(base + nn * 1024 + lane * 16);
-        else *(u16x4*)((uint16_t*)a.out + off) = *(const u16x4*)(base + nn * 512 + lane * 8);
-      }
-    }
-    st_n = 0;
-    st_off = 0;
-  };
-  auto stage_begin = [&](int bytes) __attribute__((always_inline)) {  // room for one entry; returns its LDS offset
-    if (st_n == kMaxStaged || st_off + bytes > kStageBytes) {
-      // Write the rows out.  The record of the slice's first piece, when it
-      // has one, is always the first entry, at offset 0: it stays for the
-      // merge.  Two records fit together.
-      flush();
-      if (first_entry == 0) {
-        st_n = 1;
-        st_off = kRecBytes;
-      }
-    }
-    const int off = st_off;
-    st_off += bytes;
-    return off;
-  };
-  auto stage_meta = [&](int kind, int off, long long dst) __attribute__((always_inline)) {
-    if (lane == 0) {
-      stage_kind[w][st_n] = kind | (off << 4);
-      stage_dst[w][st_n] = dst;
-    }
-    ++st_n;
-  };
 
   i32x4 qv[4];          // query group of the piece being computed
   i32x4 qE[4], qO[4];   // query groups of the segments of the next even / odd unit
@@ -638,7 +583,6 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   bool piece_first = true;
   // split segments this wave must signal: (s, g) of its first piece and of its last piece, s = -1 if none
   int arr_s0 = -1, arr_g0 = 0, arr_s1 = -1, arr_g1 = 0;
-  int own_entry = -1, own_x = -1;  // staging entry and arrival index of the record of the piece ending the slice
 
   auto begin_piece = [&](int ui, const i32x4 (&qs)[4]) __attribute__((always_inline)) {
     if (ui == 0 || cs.j == 0) {  // a new piece starts: its query group, fresh softmax state
@@ -745,41 +689,37 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     }
   };
 
-  // End of a piece: stage its rows (whole segment) or its partial record.
+  // End of a piece: its rows (whole segment) or its partial record.
   auto finish_piece = [&](int ui) __attribute__((always_inline)) {
     const bool seg_end = cs.j == cs.nus - 1;
     if (!(seg_end || ui == n - 1)) return;
     const float l_tot = xor_sum(l_part);
     const float inv = vsc / l_tot;
-    if (piece_j0 == 0 && seg_end) {  // the whole segment: final output
-      const int bytes = a.out_fp32 ? 8192 : 4096;
-      char* base = stg + stage_begin(bytes);
+    if (piece_j0 == 0 && seg_end) {  // the whole segment: final output, written straight out
+      // (these stores follow the loads of the next unit, and a wait for any
+      // later load comes a unit's computation after them)
+      if (li < G) {
+        const size_t row = ((size_t)cs.s * a.hq + (size_t)cs.g * G + li) * kHeadDim + 4 * lj;
 #pragma unroll
-      for (int nn = 0; nn < 8; ++nn) {
-        const f32x4 o = acc[nn] * inv;
-        if (a.out_fp32) {
-          *(f32x4*)(base + nn * 1024 + lane * 16) = o;
-        } else {
-          u16x4 ob;
+        for (int nn = 0; nn < 8; ++nn) {
+          const f32x4 o = acc[nn] * inv;
+          if (a.out_fp32) {
+            *(f32x4*)((float*)a.out + row + 16 * nn) = o;
+          } else {
+            u16x4 ob;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) ob[e] = f32_to_bf16_bits(o[e]);
-          *(u16x4*)(base + nn * 512 + lane * 8) = ob;
+            for (int e = 0; e < 4; ++e) ob[e] = f32_to_bf16_bits(o[e]);
+            *(u16x4*)((uint16_t*)a.out + row + 16 * nn) = ob;
+          }
         }
       }
-      stage_meta(a.out_fp32 ? 1 : 0, (int)(base - stg), ((long long)cs.s * a.hq + (long long)cs.g * G) * kHeadDim);
     } else {  // a piece of a segment cut by slice boundaries
-      char* base = stg + stage_begin(kRecBytes);
+      char* base = stg + (piece_first ? 0 : kRecBytes);
 #pragma unroll
       for (int nn = 0; nn < 8; ++nn) *(f32x4*)(base + nn * 1024 + lane * 16) = acc[nn] * inv;
       float* ml = (float*)(base + 8192 + lane * 8);
       ml[0] = m_run;
       ml[1] = l_tot;
-      if (ui == n - 1) {
-        own_entry = st_n;
-        own_x = piece_first ? 0 : 1;
-      }
-      if (piece_first) first_entry = st_n;
-      stage_meta(2, (int)(base - stg), (long long)gw * 2 + (piece_first ? 0 : 1));
       if (piece_first) {
         arr_s0 = cs.s;
         arr_g0 = cs.g;
@@ -846,8 +786,8 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   // ---- 5. merge the split pieces ----
   // Stage 1, inside the workgroup: each piece of a segment is counted on an
   // LDS counter of the segment's share of this workgroup (keyed by the share's
-  // first piece), after its owner has noted where in its LDS staging area the
-  // piece's record is.  The last arrival folds the share's pieces in order.  A segment entirely inside
+  // first piece), after its owner has written its record to its LDS.  The
+  // last arrival folds the share's pieces in order from their owners' LDS.  A segment entirely inside
   // the workgroup is then written; the share of a segment that crosses the
   // workgroup's edges is the workgroup's piece for stage 2.
   // Stage 2, across workgroups: workgroup pieces are merged in groups of
@@ -892,31 +832,19 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     p.ngroups = (p.nwp + kFanIn - 1) / kFanIn;
     return p;
   };
-  // Piece x = 0 is the slice's first split piece, x = 1 its last.  The
-  // staging entry of each, while its record is still in LDS:
-  const int ent0 = own_x == 0 ? own_entry : first_entry;
-  const int ent1 = own_x == 1 ? own_entry : -1;
+  // Piece x = 0 is the slice's first split piece, x = 1 its last; its
+  // record is at x * kRecBytes in the wave's LDS.
+  if (arr_s0 < 0 && arr_s1 < 0) return;
   Part p0 = {}, p1 = {};
   if (arr_s0 >= 0) p0 = part_of(arr_s0, arr_g0);
   if (arr_s1 >= 0) p1 = part_of(arr_s1, arr_g1);
-  flush();  // finished rows; the pieces' records stay in the staging area
-  if (arr_s0 < 0 && arr_s1 < 0) return;
-  auto entry_offset = [&](int e) __attribute__((always_inline)) {
-    return __builtin_amdgcn_readfirstlane(stage_kind[w][e]) >> 4;  // byte offset of entry e in the staging area
-  };
-  // Note where each piece's record is in the staging area, then count it
-  // (release: the directory entry and the record are visible before the
-  // count).
+  // Count each piece (release: its record is visible before the count).
   int lold0 = 0, lold1 = 0;
   if (lane == 0) {
-    if (arr_s0 >= 0) {
-      wg_dir[w][0] = entry_offset(ent0);
+    if (arr_s0 >= 0)
       lold0 = __hip_atomic_fetch_add(&wg_cnt[p0.key], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
-    }
-    if (arr_s1 >= 0) {
-      wg_dir[w][1] = entry_offset(ent1);
+    if (arr_s1 >= 0)
       lold1 = __hip_atomic_fetch_add(&wg_cnt[p1.key], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
-    }
   }
   const bool last0 = arr_s0 >= 0 && __shfl(lold0, 0) == p0.pkend - p0.pk0;
   const bool last1 = arr_s1 >= 0 && __shfl(lold1, 0) == p1.pkend - p1.pk0;
@@ -951,8 +879,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
         const int k = p.pk0 + r;
         const int x = k == p.k0 ? (p.first_slot & 1) : 0;  // the wave's first or last piece
         const int ow = __builtin_amdgcn_readfirstlane(k - wg_first);
-        const int d = __builtin_amdgcn_readfirstlane(wg_dir[ow][x]);
-        fetch_record(a, 0, (const char*)stage_lds[ow] + d, P, m, l, x0, x1);
+        fetch_record(a, 0, (const char*)stage_lds[ow] + x * kRecBytes, P, m, l, x0, x1);
       });
       if (p.nwp == 1) {  // the segment lies inside the workgroup
         write_rows(a, Fw, P, p.s, p.g);
@@ -1160,12 +1087,11 @@ int validate(const dp_decode_shape* sh, Plan* plan) {
   plan->unit_tokens = unit;
   plan->min_chunk = P ? P / unit : 1;
   // LDS per workgroup: the kernel's static arrays (tile lists, wave sums,
-  // staging of finished rows and records, the workgroup's merge counters and
-  // record directory, with 256 bytes for alignment) +
+  // each wave's two records, the workgroup's merge counters, with 256 bytes
+  // for alignment) +
   // unit prefix, context lengths and fp8 scales (dynamic)
   const size_t stat = (size_t)kWaves * kMaxUnitsPerWave * (fp8 ? 4 : 2) * sizeof(int) + kWaves * sizeof(int) +
-                      (size_t)kWaves * kStageBytes + (size_t)kWaves * kMaxStaged * (sizeof(long long) + sizeof(int)) +
-                      (size_t)kWaves * 4 * sizeof(int) + 256;
+                      (size_t)kWaves * 2 * kRecBytes + (size_t)2 * kWaves * sizeof(int) + 256;
   plan->dyn_lds = (size_t)(2 * sh->batch + 1 + 2 * sh->n_kv_heads) * 4;
   if (stat + plan->dyn_lds > kLdsBytes)
     return fail(DP_ENOTSUP, "paged_decode: %zu bytes of LDS per workgroup", stat + plan->dyn_lds);

@@ -104,7 +104,6 @@ def simulate(ctx, hkv, fp8, max_ctx, max_blocks_per_seq, partition_tokens=0, wgs
     q_rows, bt_reads, computed = [], [], []
     records = {}        # record slot -> (s, g, piece index r)
     pieces = {}         # (s, g) -> list of (wave, slot)
-    staged = {}         # wave -> its staging entries in order: ("row", None) or ("rec", slot)
     for gw in range(TW):
         u0 = gw * C
         u1 = min(u0 + C, U)
@@ -138,10 +137,8 @@ def simulate(ctx, hkv, fp8, max_ctx, max_blocks_per_seq, partition_tokens=0, wgs
             if not (seg_end or ui == n - 1):
                 return
             if state["piece_j0"] == 0 and seg_end:
-                staged.setdefault(gw, []).append(("row", None))
-                return  # whole segment: its rows, staged then written to the output
+                return  # whole segment: written straight to the output
             slot = 2 * gw + (0 if state["piece_first"] else 1)
-            staged.setdefault(gw, []).append(("rec", slot))
             assert slot not in records
             records[slot] = (cs.s, cs.g)
             pieces.setdefault((cs.s, cs.g), []).append((gw, slot))
@@ -164,29 +161,7 @@ def simulate(ctx, hkv, fp8, max_ctx, max_blocks_per_seq, partition_tokens=0, wgs
             ui += 1
         compute(ui, cs)
     return dict(B=B, TW=TW, C=C, U=U, pre=pre, q_rows=q_rows, bt_reads=bt_reads, computed=computed,
-                records=records, pieces=pieces, max_blocks_per_seq=max_blocks_per_seq, staged=staged)
-
-
-STAGE_BYTES, MAX_STAGED = 24 * 1024, 6      # a wave's LDS staging area: bytes and entries
-ROW_BYTES, REC_BYTES = 4096, 8192 + 512     # one (sequence, KV head)'s bf16 rows; one record (o, m, l)
-
-
-def flushed_mid_loop(entries, row_bytes=ROW_BYTES):
-    """Record slots a wave's staging would write out before its slice ends.
-    When the next entry does not fit, the kernel writes the staged rows out
-    and keeps the first entry if it is a record (the slice's first piece);
-    the staging must never have to drop a record."""
-    out, st_n, st_off, pending = set(), 0, 0, []
-    for kind, slot in entries:
-        size = row_bytes if kind == "row" else REC_BYTES
-        if st_n == MAX_STAGED or st_off + size > STAGE_BYTES:
-            keep = pending[:1] if pending and pending[0] is not None else []
-            out |= {x for x in pending[len(keep):] if x is not None}
-            st_n, st_off, pending = len(keep), REC_BYTES * len(keep), keep
-        assert st_off + size <= STAGE_BYTES and st_n < MAX_STAGED
-        st_n, st_off = st_n + 1, st_off + size
-        pending.append(slot)
-    return out
+                records=records, pieces=pieces, max_blocks_per_seq=max_blocks_per_seq)
 
 
 def check(sim, hkv):
@@ -294,11 +269,10 @@ def run_merge_protocol(sim, rng):
     segment is written exactly once, that no merge reads a record before it
     is published, and that every counter is zero afterwards.
 
-    Per wave, as the kernel orders it.  Stage 1: for each split piece, note
-    where its record is (its LDS staging area, or its wave slot when a
-    mid-loop flush wrote it, which then has completed) and count it on the
-    LDS counter of the segment's share of the workgroup; the share's last
-    arrival folds the share's pieces.  A segment inside the workgroup is then
+    Per wave, as the kernel orders it.  Stage 1: each split piece's record is
+    in its owner's LDS; count the piece on the LDS counter of the segment's
+    share of the workgroup; the share's last arrival folds the share's
+    pieces.  A segment inside the workgroup is then
     written.  Stage 2, for a share of a segment that crosses workgroups: read
     the group counter (an atomic load, issued before the stage-1 fold); unless
     it shows every other workgroup piece of the group arrived, publish the
@@ -412,29 +386,6 @@ def run_merge_protocol(sim, rng):
         for info in ws:
             shares[info["share"]] = len(info["share_waves"])
     assert wg_cnt == shares
-
-
-@pytest.mark.parametrize("fp8", [False, True])
-@pytest.mark.parametrize("row_bytes", [ROW_BYTES, 2 * ROW_BYTES])
-def test_records_stay_in_lds(fp8, row_bytes):
-    """A wave's split-piece records are never written out by its staging: the
-    merge reads every one from its owner's LDS.  Checked on the largest-batch
-    GPU case (4,096 short contexts: many rows per slice) and random batches,
-    with bf16 and fp32 rows."""
-    rng = np.random.default_rng(31)
-    ctx = rng.integers(0, 97, 4096)
-    ctx[rng.integers(0, 4096, 64)] = 0
-    cases = [(list(ctx), 2, int(ctx.max()), 8)]
-    for trial in range(20):
-        r = np.random.default_rng(500 + trial)
-        B = int(r.choice([3, 40, 300, 2000]))
-        max_ctx = int(r.choice([50, 300, 3000]))
-        cases.append((list(draw(r, B, max_ctx, 0.2)), int(r.choice([1, 2, 8])), max_ctx, -(-max_ctx // 16)))
-    for c, hkv, max_ctx, mbps in cases:
-        sim = simulate(c, hkv, fp8, max_ctx, mbps)
-        check(sim, hkv)
-        for entries in sim["staged"].values():
-            assert flushed_mid_loop(entries, row_bytes) == set()
 
 
 @pytest.mark.parametrize("trial", range(30))

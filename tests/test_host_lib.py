@@ -238,8 +238,8 @@ def test_workspace_and_partition_sizes(host_lib):
     (dict(kv_fp8=True, partition_tokens=32), -22), (dict(workgroups_per_cu=9), -22),
     (dict(workgroups_per_cu=-1), -22), (dict(num_blocks=0), -22), (dict(batch=-1), -22),
     (dict(batch=5000), -95), (dict(partition_tokens=32 * 257), -22),
-    # unit prefix + scales no longer fit in LDS beside the kernel's staging arrays
-    (dict(batch=4096, n_q_heads=4096, n_kv_heads=4096, num_blocks=16, max_blocks_per_seq=1, max_context_len=16), -95),
+    # unit prefix + scales no longer fit in LDS beside the kernel's static arrays
+    (dict(batch=4096, n_q_heads=16384, n_kv_heads=16384, num_blocks=16, max_blocks_per_seq=1, max_context_len=16), -95),
 ])
 def test_invalid_shapes_rejected_on_host(host_lib, kw, code):
     s = shape(host_lib, **kw)
