@@ -250,9 +250,8 @@ __device__ __forceinline__ void fold_init(Fold<NP>& F) {
 // rescaled once per round, not once per record).  The order of the sums is
 // fixed by the record indices, so the fold is bit-identical whichever wave
 // performs it.
-template <int NP, class Rec>
+template <int NP, int R = kRound<NP>, class Rec>
 __device__ __forceinline__ void fold_records(Fold<NP>& F, int n, Rec rec) {
-  constexpr int R = kRound<NP>;
   n = __builtin_amdgcn_readfirstlane(n);
   for (int r0 = 0; r0 < n; r0 += R) {
     float m[R][NP], l[R][NP];
@@ -310,30 +309,38 @@ __device__ __forceinline__ Pairs<NP> pairs_of(int lane, int npairs) {
   return P;
 }
 
-// Record u from global slot `slot`, or (own) from this wave's LDS staging
-// entry `own`: eight [lane] chunks of 4 floats (dims 16 nn + 4 lj .. + 4 of
-// head li at lane li + 16 lj), then each lane's (m, l).
+// Record u from global slot `slot`: (m, l) per head, o as [head][dim].
 template <int NP>
-__device__ __forceinline__ void fetch_record(const DecodeArgs& a, size_t slot, const char* own, const Pairs<NP>& P,
-                                             float (&m)[NP], float (&l)[NP], f32x4 (&x0)[NP], f32x4 (&x1)[NP]) {
+__device__ __forceinline__ void fetch_record(const DecodeArgs& a, size_t slot, const Pairs<NP>& P, float (&m)[NP],
+                                             float (&l)[NP], f32x4 (&x0)[NP], f32x4 (&x1)[NP]) {
   const int G = a.group;
 #pragma unroll
   for (int i = 0; i < NP; ++i) {
     const int hd = P.hd[i], d0 = P.d0[i];
-    if (own) {
-      const float* ml = (const float*)(own + 8192 + hd * 8);
-      m[i] = ml[0];
-      l[i] = ml[1];
-      const int nn = d0 >> 4, q = (d0 & 15) >> 2;
-      x0[i] = *(const f32x4*)(own + nn * 1024 + (hd + 16 * q) * 16);
-      x1[i] = *(const f32x4*)(own + nn * 1024 + (hd + 16 * (q + 1)) * 16);
-    } else {
-      coherent_load2(a.rec_ml + (slot * G + hd) * 2, m[i], l[i]);
-      const __amdgpu_buffer_rsrc_t r = record_rsrc(a.rec_o, slot, G);
-      const int bo = (hd * kHeadDim + d0) * 4;
-      x0[i] = coherent_load16(r, bo);
-      x1[i] = coherent_load16(r, bo + 16);
-    }
+    coherent_load2(a.rec_ml + (slot * G + hd) * 2, m[i], l[i]);
+    const __amdgpu_buffer_rsrc_t r = record_rsrc(a.rec_o, slot, G);
+    const int bo = (hd * kHeadDim + d0) * 4;
+    x0[i] = coherent_load16(r, bo);
+    x1[i] = coherent_load16(r, bo + 16);
+  }
+}
+
+// Record u from a wave's LDS copy `own`: eight [lane] chunks of 4 floats
+// (dims 16 nn + 4 lj .. + 4 of head li at lane li + 16 lj), then each lane's
+// (m, l).  Only LDS: a fold whose loop holds no memory load needs no wait for
+// loads issued before it.
+template <int NP>
+__device__ __forceinline__ void fetch_record_lds(const char* own, const Pairs<NP>& P, float (&m)[NP], float (&l)[NP],
+                                                 f32x4 (&x0)[NP], f32x4 (&x1)[NP]) {
+#pragma unroll
+  for (int i = 0; i < NP; ++i) {
+    const int hd = P.hd[i], d0 = P.d0[i];
+    const float* ml = (const float*)(own + 8192 + hd * 8);
+    m[i] = ml[0];
+    l[i] = ml[1];
+    const int nn = d0 >> 4, q = (d0 & 15) >> 2;
+    x0[i] = *(const f32x4*)(own + nn * 1024 + (hd + 16 * q) * 16);
+    x1[i] = *(const f32x4*)(own + nn * 1024 + (hd + 16 * (q + 1)) * 16);
   }
 }
 
@@ -850,14 +857,6 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   const bool last1 = arr_s1 >= 0 && __shfl(lold1, 0) == p1.pkend - p1.pk0;
   if (!last0 && !last1) return;
   asm volatile("" ::: "memory");  // record reads are issued after this branch resolves
-  // The workgroup's pieces that go on to stage 2 read their group counter
-  // now: the atomic's round trip overlaps the stage-1 fold.  A count showing
-  // every other workgroup piece of the group arrived cannot change.
-  int c0 = 0, c1 = 0;
-  if (lane == 0) {
-    if (last0 && p0.nwp > 1) c0 = __hip_atomic_load(group_cnt(p0.kg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (last1 && p1.nwp > 1) c1 = __hip_atomic_load(group_cnt(p1.kg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
 
   // A counter is returned to zero by its last arrival, after this wave's
   // merges: no other wave touches it again in this launch, and a store ahead
@@ -874,12 +873,13 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       // stage 1: the workgroup's pieces of the segment, in order
       Fold<NP> Fw;
       fold_init(Fw);
-      fold_records(Fw, p.pkend - p.pk0 + 1, [&](int r, float(&m)[NP], float(&l)[NP], f32x4(&x0)[NP],
-                                                f32x4(&x1)[NP]) __attribute__((always_inline)) {
+      // (at most one piece per wave of the workgroup: one round of kWaves)
+      fold_records<NP, kWaves>(Fw, p.pkend - p.pk0 + 1, [&](int r, float(&m)[NP], float(&l)[NP], f32x4(&x0)[NP],
+                                                          f32x4(&x1)[NP]) __attribute__((always_inline)) {
         const int k = p.pk0 + r;
         const int x = k == p.k0 ? (p.first_slot & 1) : 0;  // the wave's first or last piece
         const int ow = __builtin_amdgcn_readfirstlane(k - wg_first);
-        fetch_record(a, 0, (const char*)stage_lds[ow] + x * kRecBytes, P, m, l, x0, x1);
+        fetch_record_lds((const char*)stage_lds[ow] + x * kRecBytes, P, m, l, x0, x1);
       });
       if (p.nwp == 1) {  // the segment lies inside the workgroup
         write_rows(a, Fw, P, p.s, p.g);
@@ -904,10 +904,16 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
             x1[i] = ox1[i];
           }
         } else {
-          fetch_record(a, slot, nullptr, P, m, l, x0, x1);
+          fetch_record(a, slot, P, m, l, x0, x1);
         }
       };
-      if (__shfl(x == 0 ? c0 : c1, 0) != p.gn - 1) {  // not yet the group's last arrival: publish and count
+      // A group counter that already shows every other workgroup piece of
+      // the group (an atomic load, far quicker than an increment's round
+      // trip) cannot change: this workgroup's piece is the last, and it merges
+      // from registers without storing its record or counting it.
+      int c = 0;
+      if (lane == 0) c = __hip_atomic_load(group_cnt(p.kg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (__shfl(c, 0) != p.gn - 1) {  // not yet the group's last arrival: publish and count
         write_record(a, P, wslot(p.rb), wm, wl, wx0, wx1);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         int old = 0;
