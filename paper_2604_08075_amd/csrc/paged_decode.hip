@@ -207,8 +207,8 @@ __device__ __forceinline__ void store_out8(const DecodeArgs& a, size_t off, f32x
 
 // Records (o, m, l): o normalised by l, m in log2 units.  A segment cut by
 // slice boundaries is merged in two stages: first inside each workgroup,
-// from the records its waves keep in their LDS staging areas, then across
-// workgroups through the workspace.  Slots 2b and 2b + 1 hold workgroup b's
+// from the records its waves keep in LDS, then across workgroups through
+// the workspace.  Slots 2b and 2b + 1 hold workgroup b's
 // first and last piece of segments that cross its edges, and
 // 2 * workgroups + b the merged record of the group of workgroup pieces
 // whose last is workgroup b's.  Workgroup pieces are merged in groups of
@@ -394,15 +394,24 @@ struct Walker {
   int s, g, j, nus;
 };
 
+// a / d for a >= 0, d >= 1 and a quotient below 2^22 (a wave or workgroup
+// index): the float estimate is then off by at most one, and one step
+// corrects it.  rd = 1 / d, rounded.
+__device__ __forceinline__ int div_small(int a, int d, float rd) {
+  const int q = (int)((float)a * rd);
+  const int r = a - q * d;
+  return q + (r >= d ? 1 : 0) - (r < 0 ? 1 : 0);
+}
+
 template <bool FP8>
 __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a) {
   using GE = Geo<FP8>;
   constexpr int UB = GE::UB, UT = GE::UT, TILE = GE::TILE, NZ = GE::NZ;
   __shared__ int tiles_lds[kWaves][kMaxUnitsPerWave * UB];
   __shared__ int wave_sums[kWaves];
-  // Split pieces are first merged inside the workgroup: arrivals per share
-  // of a segment, keyed by the share's first piece (wave, first or last).
-  __shared__ int wg_cnt[2 * kWaves];
+  // Split pieces are first merged inside the workgroup: the segment (s, g)
+  // of each wave's first and last split piece (s = -1: none).
+  __shared__ int wg_seg[2 * kWaves][2];
   __shared__ __attribute__((aligned(16))) char stage_lds[kWaves][2 * kRecBytes];  // each wave's two records
   extern __shared__ int dyn[];  // pre[B + 1], ctxs[B], k_scale[Hkv], v_scale[Hkv]
 
@@ -441,7 +450,6 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       if (lane >= off) incl += v;
     }
     if (lane == 63) wave_sums[w] = incl;
-    if (tid < 2 * kWaves) wg_cnt[tid] = 0;
     __syncthreads();
     int run = incl - local;
     for (int k = 0; k < w; ++k) run += wave_sums[k];
@@ -459,6 +467,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   const int TW = gridDim.x * kWaves;
   int C = (U + TW - 1) / TW;
   if (C < a.min_chunk) C = a.min_chunk;
+  const float rC = 1.0f / (float)C, rCW = 1.0f / (float)(kWaves * C);  // for the merge's slice arithmetic
   const int gw = blockIdx.x * kWaves + w;
 
   // rows of empty sequences are zero
@@ -470,333 +479,335 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     }
   }
 
+  // Waves take consecutive slices: a workgroup whose first wave has no units
+  // has none at all, and leaves as a whole (a barrier follows the walk).
+  if ((int)blockIdx.x * kWaves * C >= U) return;
   const int u0 = gw * C;
   const int u1 = min(u0 + C, U);
-  if (u0 >= u1) return;  // no work; no barrier follows: waves are independent from here on
-  const int n = u1 - u0;
-
-  // ---- 2. tile indices (block id * Hkv + head) of this wave's units ----
-  int* tiles = tiles_lds[w];
-  for (int i = lane; i < n; i += 64) {
-    const int u = u0 + i;
-    int lo = 0, hi = B - 1;  // largest s with Hkv * pre[s] <= u
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (Hkv * pre[mid] <= u) lo = mid;
-      else hi = mid - 1;
-    }
-    const int s = lo;
-    const int nus = pre[s + 1] - pre[s];
-    const int r = u - Hkv * pre[s];
-    const int g = r / nus;
-    const int j = r - g * nus;
-    const int nb = (ctxs[s] + kBlock - 1) / kBlock;
-    for (int b = 0; b < UB; ++b) {
-      // a block past the sequence's end is never fetched: its lanes re-read the
-      // unit's first block (same addresses as other lanes of the same load
-      // instruction, so no extra memory traffic) and its tokens are masked
-      const int blk = j * UB + (j * UB + b < nb ? b : 0);
-      int id = a.block_tables[(size_t)s * a.max_blocks_per_seq + blk];
-      id = id < 0 ? 0 : (id > a.num_blocks_m1 ? a.num_blocks_m1 : id);
-      tiles[i * UB + b] = id * Hkv + g;
-    }
-  }
-
-  // ---- 3. per-lane operand offsets inside a tile ----
-  int kofs[8], vofs[8];
-  int kblk, vblk;  // which block of the unit this lane's K / V fragments come from
-  if constexpr (FP8) {
-    // K: MFMA m (0..3), row li = token 4m + (li & 3) of block li >> 2; fragment j = dims 64j + 16lj .. +16
-    for (int m = 0; m < 4; ++m)
-      for (int jj = 0; jj < 2; ++jj) kofs[2 * m + jj] = (4 * m + (li & 3)) * 128 + 64 * jj + 16 * lj;
-    kblk = li >> 2;
-    // V: dim 16nn + li, all 16 tokens of block lj
-    for (int nn = 0; nn < 8; ++nn) vofs[nn] = (16 * nn + li) * 16;
-    vblk = lj;
-  } else {
-    // K: MFMA m (0..1), row li = token 8((li >> 2) & 1) + 4m + (li & 3) of block li >> 3; chunk c = dims 32c + 8lj
-    for (int m = 0; m < 2; ++m)
-      for (int c = 0; c < 4; ++c) kofs[4 * m + c] = (8 * ((li >> 2) & 1) + 4 * m + (li & 3)) * 256 + 64 * c + 16 * lj;
-    kblk = li >> 3;
-    // V: dim 16nn + li, tokens 8(lj & 1) .. +8 of block lj >> 1
-    for (int nn = 0; nn < 8; ++nn) vofs[nn] = (16 * nn + li) * 32 + 16 * (lj & 1);
-    vblk = lj >> 1;
-  }
-  // query fragment c of head li: the dims its K fragment holds.  Columns past
-  // the GQA group repeat a real head; they only ever affect their own
-  // (unwritten) output columns.
-  int qoff[4];
-  for (int c = 0; c < 4; ++c) qoff[c] = FP8 ? 64 * (c >> 1) + 16 * lj + 8 * (c & 1) : 32 * c + 8 * lj;
-  const int qhead = li < G ? li : li % G;
-
-  // ---- 4. walk the slice ----
-  Walker cs;  // compute side
-  {
-    int lo = 0, hi = B - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (Hkv * pre[mid] <= u0) lo = mid;
-      else hi = mid - 1;
-    }
-    cs.s = __builtin_amdgcn_readfirstlane(lo);
-    cs.nus = __builtin_amdgcn_readfirstlane(pre[cs.s + 1] - pre[cs.s]);
-    const int r = u0 - Hkv * pre[cs.s];
-    cs.g = __builtin_amdgcn_readfirstlane(r / cs.nus);
-    cs.j = __builtin_amdgcn_readfirstlane(r - cs.g * cs.nus);
-  }
-  auto advance = [&](Walker& wk) __attribute__((always_inline)) {
-    if (++wk.j == wk.nus) {
-      wk.j = 0;
-      if (++wk.g == Hkv) {
-        wk.g = 0;
-        do {
-          ++wk.s;
-        } while (wk.s < B - 1 && pre[wk.s + 1] == pre[wk.s]);  // skip empty sequences (bounded)
-        // Stepping off the last sequence only happens to a look-ahead
-        // position past the end of the stream (never computed); it stays on
-        // the last sequence so that the query rows it prefetches exist.
-        wk.s = __builtin_amdgcn_readfirstlane(wk.s > B - 1 ? B - 1 : wk.s);
-      }
-      wk.nus = __builtin_amdgcn_readfirstlane(pre[wk.s + 1] - pre[wk.s]);
-    }
-  };
-  // Every load in the loop is unconditional, so the compiler's wait counts
-  // stay exact: a wait for one unit never drains the unit behind it.
-  auto load_q = [&](i32x4 (&qr)[4], int s, int g) __attribute__((always_inline)) {
-    const uint16_t* qrow = a.q + ((size_t)s * a.hq + (size_t)g * G + qhead) * kHeadDim;
-    for (int c = 0; c < 4; ++c) qr[c] = *(const i32x4*)(qrow + qoff[c]);
-  };
-  auto issue = [&](UnitRegs& R, int ui) __attribute__((always_inline)) {
-    const char* kb = a.k + (size_t)tiles[ui * UB + kblk] * TILE;
-    const char* vb = a.v + (size_t)tiles[ui * UB + vblk] * TILE;
-#pragma unroll
-    for (int x = 0; x < 8; ++x) R.k[x] = __builtin_nontemporal_load((const i32x4*)(kb + kofs[x]));
-#pragma unroll
-    for (int x = 0; x < 8; ++x) R.v[x] = __builtin_nontemporal_load((const i32x4*)(vb + vofs[x]));
-  };
-
-  // ---- the records of this wave's split pieces, in LDS ----
-  // At most two: the slice's first piece (x = 0) at offset 0, its last
-  // (x = 1) at kRecBytes.  Layout: eight 1 KiB chunks of o ([nn][lane], 16
-  // bytes per lane), then each lane's (m, l).  They stay there for the merge.
-  char* const stg = stage_lds[w];
-
-  i32x4 qv[4];          // query group of the piece being computed
-  i32x4 qE[4], qO[4];   // query groups of the segments of the next even / odd unit
-  float m_run = -INFINITY, l_part = 0.f, cscale = 0.f, vsc = 1.0f;
-  f32x4 acc[8];
-  for (int nn = 0; nn < 8; ++nn) acc[nn] = f32x4{0.f, 0.f, 0.f, 0.f};
-  int piece_j0 = 0, ctx_s = 0;
-  bool piece_first = true;
   // split segments this wave must signal: (s, g) of its first piece and of its last piece, s = -1 if none
   int arr_s0 = -1, arr_g0 = 0, arr_s1 = -1, arr_g1 = 0;
+  if (u0 < u1) {  // a wave without units goes straight to the merge
+    const int n = u1 - u0;
 
-  auto begin_piece = [&](int ui, const i32x4 (&qs)[4]) __attribute__((always_inline)) {
-    if (ui == 0 || cs.j == 0) {  // a new piece starts: its query group, fresh softmax state
-      piece_first = ui == 0;
-      piece_j0 = cs.j;
-      ctx_s = __builtin_amdgcn_readfirstlane(ctxs[cs.s]);
-#pragma unroll
-      for (int c = 0; c < 4; ++c) qv[c] = qs[c];
-      float ksc = 1.0f;
-      if constexpr (FP8) {
-        ksc = kscl[cs.g];
-        vsc = vscl[cs.g];
+    // ---- 2. tile indices (block id * Hkv + head) of this wave's units ----
+    int* tiles = tiles_lds[w];
+    int f_s = 0, f_nus = 1, f_g = 0, f_j = 0;  // the position of unit u0 + lane (lane 0: the slice's first unit)
+    for (int i = lane; i < n; i += 64) {
+      const int u = u0 + i;
+      int lo = 0, hi = B - 1;  // largest s with Hkv * pre[s] <= u
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (Hkv * pre[mid] <= u) lo = mid;
+        else hi = mid - 1;
       }
-      cscale = a.qk_scale_log2 * ksc;
-      m_run = -INFINITY;
-      l_part = 0.f;
-#pragma unroll
-      for (int nn = 0; nn < 8; ++nn) acc[nn] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int s = lo;
+      const int nus = pre[s + 1] - pre[s];
+      const int r = u - Hkv * pre[s];
+      const int g = r / nus;
+      const int j = r - g * nus;
+      if (i == lane) {
+        f_s = s;
+        f_nus = nus;
+        f_g = g;
+        f_j = j;
+      }
+      const int nb = (ctxs[s] + kBlock - 1) / kBlock;
+      for (int b = 0; b < UB; ++b) {
+        // a block past the sequence's end is never fetched: its lanes re-read the
+        // unit's first block (same addresses as other lanes of the same load
+        // instruction, so no extra memory traffic) and its tokens are masked
+        const int blk = j * UB + (j * UB + b < nb ? b : 0);
+        int id = a.block_tables[(size_t)s * a.max_blocks_per_seq + blk];
+        id = id < 0 ? 0 : (id > a.num_blocks_m1 ? a.num_blocks_m1 : id);
+        tiles[i * UB + b] = id * Hkv + g;
+      }
     }
-  };
 
-  auto compute_unit = [&](const UnitRegs& R) __attribute__((always_inline)) {
-    const int unit_tok0 = cs.j * UT;
-    const bool ragged = unit_tok0 + UT > ctx_s;
-    const int lane_tok0 = unit_tok0 + (FP8 ? 16 : 8) * lj;  // first unit token of this lane's scores
-
-    // S^T = K Q^T: lane (li, lj) holds scores of head li for its NZ tokens
-    float z[NZ];
+    // ---- 3. per-lane operand offsets inside a tile ----
+    int kofs[8], vofs[8];
+    int kblk, vblk;  // which block of the unit this lane's K / V fragments come from
     if constexpr (FP8) {
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int jj = 0; jj < 2; ++jj) {
-          const i32x4 raw = R.k[2 * m + jj];
-          sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(raw[0], raw[1]),
-                                                         __builtin_bit_cast(bf16x8, qv[2 * jj]), sacc, 0, 0, 0);
-          sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(raw[2], raw[3]),
-                                                         __builtin_bit_cast(bf16x8, qv[2 * jj + 1]), sacc, 0, 0,
-                                                         0);
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) z[4 * m + e] = sacc[e] * cscale;
-      }
+      // K: MFMA m (0..3), row li = token 4m + (li & 3) of block li >> 2; fragment j = dims 64j + 16lj .. +16
+      for (int m = 0; m < 4; ++m)
+        for (int jj = 0; jj < 2; ++jj) kofs[2 * m + jj] = (4 * m + (li & 3)) * 128 + 64 * jj + 16 * lj;
+      kblk = li >> 2;
+      // V: dim 16nn + li, all 16 tokens of block lj
+      for (int nn = 0; nn < 8; ++nn) vofs[nn] = (16 * nn + li) * 16;
+      vblk = lj;
     } else {
-#pragma unroll
-      for (int m = 0; m < 2; ++m) {
-        f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int c = 0; c < 4; ++c)
-          sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, R.k[4 * m + c]),
-                                                         __builtin_bit_cast(bf16x8, qv[c]), sacc, 0, 0, 0);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) z[4 * m + e] = sacc[e] * cscale;
+      // K: MFMA m (0..1), row li = token 8((li >> 2) & 1) + 4m + (li & 3) of block li >> 3; chunk c = dims 32c + 8lj
+      for (int m = 0; m < 2; ++m)
+        for (int c = 0; c < 4; ++c) kofs[4 * m + c] = (8 * ((li >> 2) & 1) + 4 * m + (li & 3)) * 256 + 64 * c + 16 * lj;
+      kblk = li >> 3;
+      // V: dim 16nn + li, tokens 8(lj & 1) .. +8 of block lj >> 1
+      for (int nn = 0; nn < 8; ++nn) vofs[nn] = (16 * nn + li) * 32 + 16 * (lj & 1);
+      vblk = lj >> 1;
+    }
+    // query fragment c of head li: the dims its K fragment holds.  Columns past
+    // the GQA group repeat a real head; they only ever affect their own
+    // (unwritten) output columns.
+    int qoff[4];
+    for (int c = 0; c < 4; ++c) qoff[c] = FP8 ? 64 * (c >> 1) + 16 * lj + 8 * (c & 1) : 32 * c + 8 * lj;
+    const int qhead = li < G ? li : li % G;
+
+    // ---- 4. walk the slice ----
+    Walker cs;  // compute side: the slice's first unit, as lane 0 located it above
+    cs.s = __builtin_amdgcn_readlane(f_s, 0);
+    cs.nus = __builtin_amdgcn_readlane(f_nus, 0);
+    cs.g = __builtin_amdgcn_readlane(f_g, 0);
+    cs.j = __builtin_amdgcn_readlane(f_j, 0);
+    auto advance = [&](Walker& wk) __attribute__((always_inline)) {
+      if (++wk.j == wk.nus) {
+        wk.j = 0;
+        if (++wk.g == Hkv) {
+          wk.g = 0;
+          do {
+            ++wk.s;
+          } while (wk.s < B - 1 && pre[wk.s + 1] == pre[wk.s]);  // skip empty sequences (bounded)
+          // Stepping off the last sequence only happens to a look-ahead
+          // position past the end of the stream (never computed); it stays on
+          // the last sequence so that the query rows it prefetches exist.
+          wk.s = __builtin_amdgcn_readfirstlane(wk.s > B - 1 ? B - 1 : wk.s);
+        }
+        wk.nus = __builtin_amdgcn_readfirstlane(pre[wk.s + 1] - pre[wk.s]);
       }
-    }
-    // live tokens among this lane's NZ tokens (all of them unless the unit is ragged)
-    const int nv = ragged ? min(max(ctx_s - lane_tok0, 0), NZ) : NZ;
-    if (ragged)
+    };
+    // Every load in the loop is unconditional, so the compiler's wait counts
+    // stay exact: a wait for one unit never drains the unit behind it.
+    auto load_q = [&](i32x4 (&qr)[4], int s, int g) __attribute__((always_inline)) {
+      const uint16_t* qrow = a.q + ((size_t)s * a.hq + (size_t)g * G + qhead) * kHeadDim;
+      for (int c = 0; c < 4; ++c) qr[c] = *(const i32x4*)(qrow + qoff[c]);
+    };
+    auto issue = [&](UnitRegs& R, int ui) __attribute__((always_inline)) {
+      const char* kb = a.k + (size_t)tiles[ui * UB + kblk] * TILE;
+      const char* vb = a.v + (size_t)tiles[ui * UB + vblk] * TILE;
 #pragma unroll
-      for (int e = 0; e < NZ; ++e)
-        if (e >= nv) z[e] = -INFINITY;
+      for (int x = 0; x < 8; ++x) R.k[x] = __builtin_nontemporal_load((const i32x4*)(kb + kofs[x]));
+#pragma unroll
+      for (int x = 0; x < 8; ++x) R.v[x] = __builtin_nontemporal_load((const i32x4*)(vb + vofs[x]));
+    };
 
-    // online softmax (base 2) for head li over this unit's tokens
-    float bmax = z[0];
-    for (int e = 1; e < NZ; ++e) bmax = fmaxf(bmax, z[e]);
-    bmax = xor_max(bmax);
-    const float m_new = fmaxf(m_run, bmax);
-    if (__builtin_amdgcn_ballot_w64(m_new > m_run) != 0) {  // some head's max grew: rescale
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      l_part *= alpha;
-#pragma unroll
-      for (int nn = 0; nn < 8; ++nn) acc[nn] *= alpha;
-      m_run = m_new;
-    }
-    bf16x8 p[NZ / 8];
-    float psum = 0.f;
-#pragma unroll
-    for (int e = 0; e < NZ; ++e) {
-      const __bf16 pe = (__bf16)__builtin_amdgcn_exp2f(z[e] - m_run);
-      p[e >> 3][e & 7] = pe;
-      psum += (float)pe;
-    }
-    l_part += psum;
+    // ---- the records of this wave's split pieces, in LDS ----
+    // At most two: the slice's first piece (x = 0) at offset 0, its last
+    // (x = 1) at kRecBytes.  Layout: eight 1 KiB chunks of o ([nn][lane], 16
+    // bytes per lane), then each lane's (m, l).  They stay there for the merge.
+    char* const stg = stage_lds[w];
 
-    // O^T += V^T P^T.  A V fragment is 16 bytes: 8 bf16 tokens, or 16 fp8
-    // tokens (8 for each of two MFMAs); dead tokens are zeroed on the raw words.
-    unsigned vmask[4] = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
-    if (ragged)
+    i32x4 qv[4];          // query group of the piece being computed
+    i32x4 qE[4], qO[4];   // query groups of the segments of the next even / odd unit
+    float m_run = -INFINITY, l_part = 0.f, cscale = 0.f, vsc = 1.0f;
+    f32x4 acc[8];
+    for (int nn = 0; nn < 8; ++nn) acc[nn] = f32x4{0.f, 0.f, 0.f, 0.f};
+    int piece_j0 = 0, ctx_s = 0;
+    bool piece_first = true;
+
+    auto begin_piece = [&](int ui, const i32x4 (&qs)[4]) __attribute__((always_inline)) {
+      if (ui == 0 || cs.j == 0) {  // a new piece starts: its query group, fresh softmax state
+        piece_first = ui == 0;
+        piece_j0 = cs.j;
+        ctx_s = __builtin_amdgcn_readfirstlane(ctxs[cs.s]);
 #pragma unroll
-      for (int wd = 0; wd < 4; ++wd) vmask[wd] = live_mask<FP8 ? 1 : 2>(wd, nv);
+        for (int c = 0; c < 4; ++c) qv[c] = qs[c];
+        float ksc = 1.0f;
+        if constexpr (FP8) {
+          ksc = kscl[cs.g];
+          vsc = vscl[cs.g];
+        }
+        cscale = a.qk_scale_log2 * ksc;
+        m_run = -INFINITY;
+        l_part = 0.f;
 #pragma unroll
-    for (int nn = 0; nn < 8; ++nn) {
-      i32x4 raw = R.v[nn];
+        for (int nn = 0; nn < 8; ++nn) acc[nn] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    };
+
+    auto compute_unit = [&](const UnitRegs& R) __attribute__((always_inline)) {
+      const int unit_tok0 = cs.j * UT;
+      const bool ragged = unit_tok0 + UT > ctx_s;
+      const int lane_tok0 = unit_tok0 + (FP8 ? 16 : 8) * lj;  // first unit token of this lane's scores
+
+      // S^T = K Q^T: lane (li, lj) holds scores of head li for its NZ tokens
+      float z[NZ];
+      if constexpr (FP8) {
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int jj = 0; jj < 2; ++jj) {
+            const i32x4 raw = R.k[2 * m + jj];
+            sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(raw[0], raw[1]),
+                                                           __builtin_bit_cast(bf16x8, qv[2 * jj]), sacc, 0, 0, 0);
+            sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(raw[2], raw[3]),
+                                                           __builtin_bit_cast(bf16x8, qv[2 * jj + 1]), sacc, 0, 0,
+                                                           0);
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) z[4 * m + e] = sacc[e] * cscale;
+        }
+      } else {
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
+          f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, R.k[4 * m + c]),
+                                                           __builtin_bit_cast(bf16x8, qv[c]), sacc, 0, 0, 0);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) z[4 * m + e] = sacc[e] * cscale;
+        }
+      }
+      // live tokens among this lane's NZ tokens (all of them unless the unit is ragged)
+      const int nv = ragged ? min(max(ctx_s - lane_tok0, 0), NZ) : NZ;
       if (ragged)
 #pragma unroll
-        for (int wd = 0; wd < 4; ++wd) raw[wd] &= (int)vmask[wd];
-      if constexpr (FP8) {
-        acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(raw[0], raw[1]), p[0], acc[nn], 0, 0, 0);
-        acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(raw[2], raw[3]), p[1], acc[nn], 0, 0, 0);
-      } else {
-        acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, raw), p[0], acc[nn], 0, 0, 0);
-      }
-    }
-  };
+        for (int e = 0; e < NZ; ++e)
+          if (e >= nv) z[e] = -INFINITY;
 
-  // End of a piece: its rows (whole segment) or its partial record.
-  auto finish_piece = [&](int ui) __attribute__((always_inline)) {
-    const bool seg_end = cs.j == cs.nus - 1;
-    if (!(seg_end || ui == n - 1)) return;
-    const float l_tot = xor_sum(l_part);
-    const float inv = vsc / l_tot;
-    if (piece_j0 == 0 && seg_end) {  // the whole segment: final output, written straight out
-      // (these stores follow the loads of the next unit, and a wait for any
-      // later load comes a unit's computation after them)
-      if (li < G) {
-        const size_t row = ((size_t)cs.s * a.hq + (size_t)cs.g * G + li) * kHeadDim + 4 * lj;
+      // online softmax (base 2) for head li over this unit's tokens
+      float bmax = z[0];
+      for (int e = 1; e < NZ; ++e) bmax = fmaxf(bmax, z[e]);
+      bmax = xor_max(bmax);
+      const float m_new = fmaxf(m_run, bmax);
+      if (__builtin_amdgcn_ballot_w64(m_new > m_run) != 0) {  // some head's max grew: rescale
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        l_part *= alpha;
 #pragma unroll
-        for (int nn = 0; nn < 8; ++nn) {
-          const f32x4 o = acc[nn] * inv;
-          if (a.out_fp32) {
-            *(f32x4*)((float*)a.out + row + 16 * nn) = o;
-          } else {
-            u16x4 ob;
+        for (int nn = 0; nn < 8; ++nn) acc[nn] *= alpha;
+        m_run = m_new;
+      }
+      bf16x8 p[NZ / 8];
+      float psum = 0.f;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) ob[e] = f32_to_bf16_bits(o[e]);
-            *(u16x4*)((uint16_t*)a.out + row + 16 * nn) = ob;
-          }
+      for (int e = 0; e < NZ; ++e) {
+        const __bf16 pe = (__bf16)__builtin_amdgcn_exp2f(z[e] - m_run);
+        p[e >> 3][e & 7] = pe;
+        psum += (float)pe;
+      }
+      l_part += psum;
+
+      // O^T += V^T P^T.  A V fragment is 16 bytes: 8 bf16 tokens, or 16 fp8
+      // tokens (8 for each of two MFMAs); dead tokens are zeroed on the raw words.
+      unsigned vmask[4] = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
+      if (ragged)
+#pragma unroll
+        for (int wd = 0; wd < 4; ++wd) vmask[wd] = live_mask<FP8 ? 1 : 2>(wd, nv);
+#pragma unroll
+      for (int nn = 0; nn < 8; ++nn) {
+        i32x4 raw = R.v[nn];
+        if (ragged)
+#pragma unroll
+          for (int wd = 0; wd < 4; ++wd) raw[wd] &= (int)vmask[wd];
+        if constexpr (FP8) {
+          acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(raw[0], raw[1]), p[0], acc[nn], 0, 0, 0);
+          acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(raw[2], raw[3]), p[1], acc[nn], 0, 0, 0);
+        } else {
+          acc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, raw), p[0], acc[nn], 0, 0, 0);
         }
       }
-    } else {  // a piece of a segment cut by slice boundaries
-      char* base = stg + (piece_first ? 0 : kRecBytes);
-#pragma unroll
-      for (int nn = 0; nn < 8; ++nn) *(f32x4*)(base + nn * 1024 + lane * 16) = acc[nn] * inv;
-      float* ml = (float*)(base + 8192 + lane * 8);
-      ml[0] = m_run;
-      ml[1] = l_tot;
-      if (piece_first) {
-        arr_s0 = cs.s;
-        arr_g0 = cs.g;
-      } else {
-        arr_s1 = cs.s;
-        arr_g1 = cs.g;
-      }
-    }
-  };
+    };
 
-  // One unit in flight while the previous one is computed.  Per step, in
-  // program order: the K and V tiles of unit u+1; at the start of a piece,
-  // the query group of unit u's segment copied out of the ring slot of u's
-  // parity; the computation of unit u; then, only if unit u+2 starts a
-  // segment, its query group loaded into that slot.  The loop is unrolled by
-  // two so that the unit buffers and query slots are static, runs pairs of
-  // units with no exit in its body, and peels the last unit or two: with an
-  // exit inside the body, or a conditional load placed before a wait that it
-  // would join, the compiler's wait counts turn conservative and it drains
-  // every load in flight.
-  Walker w1 = cs, w2;  // positions of units u+1 and u+2
-  advance(w1);
-  w2 = w1;
-  advance(w2);
-  UnitRegs RA, RB;
-  load_q(qE, cs.s, cs.g);
-  load_q(qO, w1.s, w1.g);
-  issue(RA, 0);
-  auto step = [&](UnitRegs& cur, UnitRegs& nxt, i32x4 (&qs)[4], int ui) __attribute__((always_inline)) {
-    issue(nxt, ui + 1);
-    // keep the compiler's scheduler from hoisting the computation of unit u
-    // above these loads (it would wait for unit u before issuing unit u+1)
-    __builtin_amdgcn_sched_barrier(0);
-    begin_piece(ui, qs);
-    compute_unit(cur);
-    // Unit u's operands are consumed.  If unit u+2 starts a segment, load its
-    // query group into the slot just freed: a full step passes before any
-    // wait can cover this (conditional) load.
-    if (w2.j == 0) load_q(qs, w2.s, w2.g);
-    finish_piece(ui);
-    cs = w1;
-    w1 = w2;
-    advance(w2);
-  };
-  auto last = [&](UnitRegs& cur, const i32x4 (&qs)[4], int ui) __attribute__((always_inline)) {
-    begin_piece(ui, qs);
-    compute_unit(cur);
-    finish_piece(ui);
-  };
-  int ui = 0;
-  for (; ui + 2 < n; ui += 2) {
-    step(RA, RB, qE, ui);
-    step(RB, RA, qO, ui + 1);
-  }
-  if (ui + 1 < n) {  // two units left: the last one lands in RB; move it (and its query slot) over
-    step(RA, RB, qE, ui);
-    ++ui;
-    RA = RB;
+    // End of a piece: its rows (whole segment) or its partial record.
+    auto finish_piece = [&](int ui) __attribute__((always_inline)) {
+      const bool seg_end = cs.j == cs.nus - 1;
+      if (!(seg_end || ui == n - 1)) return;
+      const float l_tot = xor_sum(l_part);
+      const float inv = vsc / l_tot;
+      if (piece_j0 == 0 && seg_end) {  // the whole segment: final output, written straight out
+        // (these stores follow the loads of the next unit, and a wait for any
+        // later load comes a unit's computation after them)
+        if (li < G) {
+          const size_t row = ((size_t)cs.s * a.hq + (size_t)cs.g * G + li) * kHeadDim + 4 * lj;
 #pragma unroll
-    for (int c = 0; c < 4; ++c) qE[c] = qO[c];
+          for (int nn = 0; nn < 8; ++nn) {
+            const f32x4 o = acc[nn] * inv;
+            if (a.out_fp32) {
+              *(f32x4*)((float*)a.out + row + 16 * nn) = o;
+            } else {
+              u16x4 ob;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) ob[e] = f32_to_bf16_bits(o[e]);
+              *(u16x4*)((uint16_t*)a.out + row + 16 * nn) = ob;
+            }
+          }
+        }
+      } else {  // a piece of a segment cut by slice boundaries
+        char* base = stg + (piece_first ? 0 : kRecBytes);
+#pragma unroll
+        for (int nn = 0; nn < 8; ++nn) *(f32x4*)(base + nn * 1024 + lane * 16) = acc[nn] * inv;
+        float* ml = (float*)(base + 8192 + lane * 8);
+        ml[0] = m_run;
+        ml[1] = l_tot;
+        if (piece_first) {
+          arr_s0 = cs.s;
+          arr_g0 = cs.g;
+        } else {
+          arr_s1 = cs.s;
+          arr_g1 = cs.g;
+        }
+      }
+    };
+
+    // One unit in flight while the previous one is computed.  Per step, in
+    // program order: the K and V tiles of unit u+1; at the start of a piece,
+    // the query group of unit u's segment copied out of the ring slot of u's
+    // parity; the computation of unit u; then, only if unit u+2 starts a
+    // segment, its query group loaded into that slot.  The loop is unrolled by
+    // two so that the unit buffers and query slots are static, runs pairs of
+    // units with no exit in its body, and peels the last unit or two: with an
+    // exit inside the body, or a conditional load placed before a wait that it
+    // would join, the compiler's wait counts turn conservative and it drains
+    // every load in flight.
+    Walker w1 = cs, w2;  // positions of units u+1 and u+2
+    advance(w1);
+    w2 = w1;
+    advance(w2);
+    UnitRegs RA, RB;
+    load_q(qE, cs.s, cs.g);
+    load_q(qO, w1.s, w1.g);
+    issue(RA, 0);
+    auto step = [&](UnitRegs& cur, UnitRegs& nxt, i32x4 (&qs)[4], int ui) __attribute__((always_inline)) {
+      issue(nxt, ui + 1);
+      // keep the compiler's scheduler from hoisting the computation of unit u
+      // above these loads (it would wait for unit u before issuing unit u+1)
+      __builtin_amdgcn_sched_barrier(0);
+      begin_piece(ui, qs);
+      compute_unit(cur);
+      // Unit u's operands are consumed.  If unit u+2 starts a segment, load its
+      // query group into the slot just freed: a full step passes before any
+      // wait can cover this (conditional) load.
+      if (w2.j == 0) load_q(qs, w2.s, w2.g);
+      finish_piece(ui);
+      cs = w1;
+      w1 = w2;
+      advance(w2);
+    };
+    auto last = [&](UnitRegs& cur, const i32x4 (&qs)[4], int ui) __attribute__((always_inline)) {
+      begin_piece(ui, qs);
+      compute_unit(cur);
+      finish_piece(ui);
+    };
+    int ui = 0;
+    for (; ui + 2 < n; ui += 2) {
+      step(RA, RB, qE, ui);
+      step(RB, RA, qO, ui + 1);
+    }
+    if (ui + 1 < n) {  // two units left: the last one lands in RB; move it (and its query slot) over
+      step(RA, RB, qE, ui);
+      ++ui;
+      RA = RB;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) qE[c] = qO[c];
+    }
+    last(RA, qE, ui);
   }
-  last(RA, qE, ui);
 
   // ---- 5. merge the split pieces ----
-  // Stage 1, inside the workgroup: each piece of a segment is counted on an
-  // LDS counter of the segment's share of this workgroup (keyed by the share's
-  // first piece), after its owner has written its record to its LDS.  The
-  // last arrival folds the share's pieces in order from their owners' LDS.  A segment entirely inside
-  // the workgroup is then written; the share of a segment that crosses the
-  // workgroup's edges is the workgroup's piece for stage 2.
+  // Stage 1, inside the workgroup: after a barrier every wave's records are
+  // in LDS, and the workgroup's shares of cut segments are merged at once,
+  // each by one wave, which folds the share's pieces in order from their
+  // owners' LDS.  A segment entirely inside the workgroup is then written;
+  // the share of a segment that crosses the workgroup's edges is the
+  // workgroup's piece for stage 2.
   // Stage 2, across workgroups: workgroup pieces are merged in groups of
   // kFanIn consecutive ones, then the groups, by the last arrival on
   // device-wide counters (the workgroup of a group's last piece, of a
@@ -812,7 +823,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   const size_t rec_wg = 0;                             // workgroup piece slots
   const size_t rec_grp = rec_wg + (size_t)2 * nwg;     // group record slots
   struct Part {
-    int s, g, k0, first_slot, pk0, pkend, key;         // the segment's waves; this workgroup's share of them
+    int s, g, k0, first_slot, pk0, pkend;              // the segment's waves; this workgroup's share of them
     int bk0, bkend, nwp, first_wslot, rb, gfirst, gn, kg, ngroups;  // its workgroups
   };
   auto part_of = [&](int s, int g) __attribute__((always_inline)) {
@@ -822,14 +833,13 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     const int a0 = __builtin_amdgcn_readfirstlane(Hkv * pre[s] + g * nus);  // first unit of the segment
     p.s = s;
     p.g = g;
-    p.k0 = a0 / C;
-    const int kend = (a0 + nus - 1) / C;
+    p.k0 = div_small(a0, C, rC);
+    const int kend = div_small(a0 + nus - 1, C, rC);
     p.first_slot = 2 * p.k0 + (a0 > p.k0 * C ? 1 : 0);
     p.pk0 = max(p.k0, wg_first);
     p.pkend = min(kend, wg_first + kWaves - 1);
-    p.key = 2 * (p.pk0 - wg_first) + (p.pk0 == p.k0 ? (p.first_slot & 1) : 0);
-    p.bk0 = a0 / CW;
-    p.bkend = (a0 + nus - 1) / CW;
+    p.bk0 = div_small(a0, CW, rCW);
+    p.bkend = div_small(a0 + nus - 1, CW, rCW);
     p.nwp = p.bkend - p.bk0 + 1;
     p.first_wslot = 2 * p.bk0 + (a0 > p.bk0 * CW ? 1 : 0);
     p.rb = (int)blockIdx.x - p.bk0;
@@ -839,37 +849,81 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     p.ngroups = (p.nwp + kFanIn - 1) / kFanIn;
     return p;
   };
-  // Piece x = 0 is the slice's first split piece, x = 1 its last; its
-  // record is at x * kRecBytes in the wave's LDS.
-  if (arr_s0 < 0 && arr_s1 < 0) return;
-  Part p0 = {}, p1 = {};
-  if (arr_s0 >= 0) p0 = part_of(arr_s0, arr_g0);
-  if (arr_s1 >= 0) p1 = part_of(arr_s1, arr_g1);
-  // Count each piece (release: its record is visible before the count).
-  int lold0 = 0, lold1 = 0;
+  // Piece x = 0 is a slice's first split piece, x = 1 its last; its record
+  // is at x * kRecBytes in the wave's LDS.
   if (lane == 0) {
-    if (arr_s0 >= 0)
-      lold0 = __hip_atomic_fetch_add(&wg_cnt[p0.key], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
-    if (arr_s1 >= 0)
-      lold1 = __hip_atomic_fetch_add(&wg_cnt[p1.key], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
+    wg_seg[2 * w][0] = arr_s0;
+    wg_seg[2 * w][1] = arr_g0;
+    wg_seg[2 * w + 1][0] = arr_s1;
+    wg_seg[2 * w + 1][1] = arr_g1;
   }
-  const bool last0 = arr_s0 >= 0 && __shfl(lold0, 0) == p0.pkend - p0.pk0;
-  const bool last1 = arr_s1 >= 0 && __shfl(lold1, 0) == p1.pkend - p1.pk0;
-  if (!last0 && !last1) return;
-  asm volatile("" ::: "memory");  // record reads are issued after this branch resolves
+  // Every record and entry of the workgroup is in LDS after this barrier (it
+  // waits for LDS accesses only, not for the rows' stores to memory).
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+  // The shares are the runs of equal segments among the entries (wave, x),
+  // in order: at most kWaves + 1, as each crosses one of the workgroup's
+  // kWaves + 1 slice boundaries.  Share i goes to wave min(pos, kWaves - 1),
+  // pos = 0 for the first share, 1 for the last, i + 1 for the others: the
+  // only shares that can cross the workgroup's edges and go on to stage 2,
+  // the first and the last, run on different waves.
+  int es[2 * kWaves], eg[2 * kWaves];
+#pragma unroll
+  for (int e = 0; e < 2 * kWaves; ++e) {
+    es[e] = __builtin_amdgcn_readfirstlane(wg_seg[e][0]);
+    eg[e] = __builtin_amdgcn_readfirstlane(wg_seg[e][1]);
+  }
+  int nsh = 0;
+  {
+    int ps = -1, pg = 0;
+#pragma unroll
+    for (int e = 0; e < 2 * kWaves; ++e)
+      if (es[e] >= 0) {
+        if (es[e] != ps || eg[e] != pg) ++nsh;
+        ps = es[e];
+        pg = eg[e];
+      }
+  }
+  int mine = 0, ms0 = 0, mg0 = 0, ms1 = 0, mg1 = 0;  // this wave's shares, in order
+  {
+    int ps = -1, pg = 0, i = -1;
+#pragma unroll
+    for (int e = 0; e < 2 * kWaves; ++e)
+      if (es[e] >= 0) {
+        if (es[e] != ps || eg[e] != pg) {
+          ++i;
+          const int pos = i == 0 ? 0 : (i == nsh - 1 ? 1 : i + 1);
+          if (min(pos, kWaves - 1) == w) {
+            if (mine == 0) {
+              ms0 = es[e];
+              mg0 = eg[e];
+            } else {
+              ms1 = es[e];
+              mg1 = eg[e];
+            }
+            ++mine;
+          }
+        }
+        ps = es[e];
+        pg = eg[e];
+      }
+  }
+  if (mine == 0) return;
 
-  // A counter is returned to zero by its last arrival, after this wave's
-  // merges: no other wave touches it again in this launch, and a store ahead
-  // of the record loads would make their wait include the store's
-  // write-through (a wave's memory counter retires loads and stores in issue
-  // order).  Bit x: group counter of piece x; bit 2 + x: its segment counter.
-  unsigned rezero = 0;
+  // A device-wide counter is returned to zero by its last arrival, after
+  // this wave's merges: no other wave touches it again in this launch, and a
+  // store ahead of the record loads would make their wait include the
+  // store's write-through (a wave's memory counter retires loads and stores
+  // in issue order).  The group and segment counters of the wave's shares
+  // x = 0, 1 that it was the last arrival of (-1: none; scalars, as an array
+  // indexed by x would live in scratch memory):
+  int rz_g0 = -1, rz_g1 = -1, rz_s0 = -1, rz_s1 = -1;
   auto merge = [&](auto np_c) __attribute__((always_inline)) {
     constexpr int NP = decltype(np_c)::value;
     const Pairs<NP> P = pairs_of<NP>(lane, G * 16);
-    for (int x = 0; x < 2; ++x) {
-      if (!(x == 0 ? last0 : last1)) continue;
-      const Part p = x == 0 ? p0 : p1;
+    for (int x = 0; x < mine; ++x) {
+      const Part p = part_of(x == 0 ? ms0 : ms1, x == 0 ? mg0 : mg1);
       // stage 1: the workgroup's pieces of the segment, in order
       Fold<NP> Fw;
       fold_init(Fw);
@@ -921,7 +975,8 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
         if (__shfl(old, 0) != p.gn - 1) continue;
         asm volatile("" ::: "memory");  // record loads are issued after this branch resolves
       }
-      rezero |= 1u << x;
+      if (x == 0) rz_g0 = p.kg;
+      else rz_g1 = p.kg;
       // the group's workgroup pieces, in order (this workgroup's from registers)
       const int own_u = p.rb - p.gfirst;
       Fold<NP> Fg;
@@ -957,7 +1012,8 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
         if (__shfl(old, 0) != p.ngroups - 1) continue;
       }
       asm volatile("" ::: "memory");  // group record loads are issued after this branch resolves
-      rezero |= 4u << x;
+      if (x == 0) rz_s0 = p.bkend;
+      else rz_s1 = p.bkend;
       Fold<NP> F;
       fold_init(F);
       fold_records(F, p.ngroups, [&](int u, float(&m)[NP], float(&l)[NP], f32x4(&x0)[NP], f32x4(&x1)[NP])
@@ -972,10 +1028,10 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   else
     merge(std::integral_constant<int, 2>{});
   if (lane == 0) {
-    if (rezero & 1u) __hip_atomic_store(group_cnt(p0.kg), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (rezero & 2u) __hip_atomic_store(group_cnt(p1.kg), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (rezero & 4u) __hip_atomic_store(seg_cnt(p0.bkend), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (rezero & 8u) __hip_atomic_store(seg_cnt(p1.bkend), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (rz_g0 >= 0) __hip_atomic_store(group_cnt(rz_g0), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (rz_g1 >= 0) __hip_atomic_store(group_cnt(rz_g1), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (rz_s0 >= 0) __hip_atomic_store(seg_cnt(rz_s0), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (rz_s1 >= 0) __hip_atomic_store(seg_cnt(rz_s1), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -1097,7 +1153,7 @@ int validate(const dp_decode_shape* sh, Plan* plan) {
   // for alignment) +
   // unit prefix, context lengths and fp8 scales (dynamic)
   const size_t stat = (size_t)kWaves * kMaxUnitsPerWave * (fp8 ? 4 : 2) * sizeof(int) + kWaves * sizeof(int) +
-                      (size_t)kWaves * 2 * kRecBytes + (size_t)2 * kWaves * sizeof(int) + 256;
+                      (size_t)kWaves * 2 * kRecBytes + (size_t)4 * kWaves * sizeof(int) + 256;
   plan->dyn_lds = (size_t)(2 * sh->batch + 1 + 2 * sh->n_kv_heads) * 4;
   if (stat + plan->dyn_lds > kLdsBytes)
     return fail(DP_ENOTSUP, "paged_decode: %zu bytes of LDS per workgroup", stat + plan->dyn_lds);

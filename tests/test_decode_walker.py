@@ -171,7 +171,7 @@ def check(sim, hkv):
     for s, blk, nb in sim["bt_reads"]:
         assert 0 <= blk < nb <= sim["max_blocks_per_seq"], (s, blk, nb)
     assert sorted(sim["computed"]) == list(range(sim["U"]))
-    counters_group, counters_seg, shares = set(), set(), set()
+    counters_group, counters_seg = set(), set()
     nwg = TW // WAVES
     CW = WAVES * C
     for (s, g), got in sim["pieces"].items():
@@ -185,12 +185,6 @@ def check(sim, hkv):
         assert sorted(by_wave) == list(range(k0, kend + 1))
         for r in range(np_):
             assert by_wave[k0 + r] == (first_slot if r == 0 else 2 * (k0 + r))
-        # stage 1: one LDS counter per share of a workgroup, keyed by its first piece
-        for b in range(k0 // WAVES, kend // WAVES + 1):
-            pk0 = max(k0, b * WAVES)
-            key = 2 * (pk0 - b * WAVES) + ((first_slot & 1) if pk0 == k0 else 0)
-            assert 0 <= key < 2 * WAVES and (b, key) not in shares
-            shares.add((b, key))
         # stage 2: workgroup pieces, groups of FAN_IN, device-wide counters per workgroup
         bk0, bkend = a0 // CW, (a0 + nus - 1) // CW
         nwp = bkend - bk0 + 1
@@ -208,6 +202,23 @@ def check(sim, hkv):
         counters_seg.add(bkend)
     for slot in sim["records"]:
         assert 0 <= slot < 2 * TW
+    # stage 1: every share of a workgroup goes to exactly one of its waves, no
+    # wave gets more than two (the kernel holds two), and the first and last
+    # shares, the only ones that can cross the workgroup's edges, go to
+    # different waves
+    for b, entries in workgroup_entries(sim).items():
+        segs = [e for e in entries if e is not None]
+        runs = [seg for i, seg in enumerate(segs) if i == 0 or seg != segs[i - 1]]
+        assert len(runs) == len(set(runs)) <= WAVES + 1
+        got = assign_shares(entries)
+        assert sorted(x for v in got.values() for x in v) == sorted(runs)
+        assert all(len(v) <= 2 for v in got.values())
+        if len(runs) >= 2:
+            assert [w for w, v in got.items() if runs[0] in v] != [w for w, v in got.items() if runs[-1] in v]
+        for seg in runs:  # a share that crosses an edge of the workgroup is its first or last
+            others = [k for k, _ in sim["pieces"][seg] if k // WAVES != b]
+            if others:
+                assert seg in (runs[0], runs[-1])
 
 
 def draw(rng, B, max_ctx, p_empty):
@@ -263,6 +274,37 @@ def test_benchmark_shapes():
 
 # ---------------------------------------------------------------- end-of-slice merge protocol
 
+def assign_shares(entries):
+    """The kernel's split of a workgroup's shares over its waves.  entries[2w + x]
+    is the segment of wave w's first (x = 0) or last (x = 1) split piece, or
+    None.  Shares are the runs of equal segments among the entries, in order;
+    share i goes to wave min(pos, WAVES - 1), pos = 0 for the first, 1 for the
+    last, i + 1 for the others."""
+    starts, prev = [], None
+    for e, seg in enumerate(entries):
+        if seg is None:
+            continue
+        if seg != prev:
+            starts.append(e)
+        prev = seg
+    out = {w: [] for w in range(WAVES)}
+    for i, e in enumerate(starts):
+        pos = 0 if i == 0 else (1 if i == len(starts) - 1 else i + 1)
+        out[min(pos, WAVES - 1)].append(entries[e])
+    return out
+
+
+def workgroup_entries(sim):
+    """entries (as assign_shares takes them) of every workgroup that has units."""
+    C, U = sim["C"], sim["U"]
+    nwg = sim["TW"] // WAVES
+    ents = {b: [None] * (2 * WAVES) for b in range(nwg) if b * WAVES * C < U}
+    for seg, got in sim["pieces"].items():
+        for k, slot in got:
+            ents[k // WAVES][2 * (k % WAVES) + (slot & 1)] = seg
+    return ents
+
+
 def run_merge_protocol(sim, rng):
     """Play the kernel's end-of-slice protocol for every split piece, with the
     waves' steps interleaved in a random order, and check that every cut
@@ -270,70 +312,65 @@ def run_merge_protocol(sim, rng):
     is published, and that every counter is zero afterwards.
 
     Per wave, as the kernel orders it.  Stage 1: each split piece's record is
-    in its owner's LDS; count the piece on the LDS counter of the segment's
-    share of the workgroup; the share's last arrival folds the share's
-    pieces.  A segment inside the workgroup is then
-    written.  Stage 2, for a share of a segment that crosses workgroups: read
-    the group counter (an atomic load, issued before the stage-1 fold); unless
+    in its owner's LDS; the workgroup's waves meet at a barrier (a wave
+    without units too); then each share of a cut segment is merged by the
+    wave assign_shares gives it, which folds the share's pieces.  A segment
+    inside the workgroup is then written.  Stage 2, for a share of a segment
+    that crosses workgroups: read the group counter (an atomic load); unless
     it shows every other workgroup piece of the group arrived, publish the
-    workgroup piece and count it; the group's last arrival folds the group and
-    either writes the segment or goes through the segment counter (load, then
-    group record and increment unless every other group is done).  Last,
+    workgroup piece and count it; the group's last arrival folds the group
+    and either writes the segment or goes through the segment counter (load,
+    then group record and increment unless every other group is done).  Last,
     after a step of its own, the wave returns to zero every device-wide
     counter it was the last arrival of.  No wave may read or count a counter
     between its last arrival and that reset."""
-    C, pre, hkv, TW = sim["C"], sim["pre"], sim["hkv"], sim["TW"]
+    C, pre, hkv = sim["C"], sim["pre"], sim["hkv"]
     CW = WAVES * C
-    waves = {}
+    info_of = {}  # (workgroup, segment) -> the share's stage-2 facts
+    pieces_of = {}  # wave -> its split pieces' segments
     for (s, g), got in sim["pieces"].items():
         nus = pre[s + 1] - pre[s]
         a0 = hkv * pre[s] + g * nus
-        k0, kend = a0 // C, (a0 + nus - 1) // C
-        first_slot = 2 * k0 + (1 if a0 > k0 * C else 0)
         bk0, bkend = a0 // CW, (a0 + nus - 1) // CW
         nwp = bkend - bk0 + 1
-        for k in range(k0, kend + 1):
+        for k, _ in got:
             b = k // WAVES
-            pk0, pkend = max(k0, b * WAVES), min(kend, b * WAVES + WAVES - 1)
             rb = b - bk0
             gfirst = rb - rb % FAN_IN
             gn = min(nwp, gfirst + FAN_IN) - gfirst
-            waves.setdefault(k, []).append(dict(
-                seg=(s, g), k=k, share=(b, 2 * (pk0 - b * WAVES) + ((first_slot & 1) if pk0 == k0 else 0)),
-                share_waves=list(range(pk0, pkend + 1)), nwp=nwp, rb=rb, gfirst=gfirst, gn=gn,
-                kg=bk0 + gfirst + gn - 1, ngroups=-(-nwp // FAN_IN), bkend=bkend))
-    wg_cnt, group_cnt, seg_cnt = {}, {}, {}
+            info_of[(b, (s, g))] = dict(seg=(s, g), nwp=nwp, rb=rb, gfirst=gfirst, gn=gn,
+                                        kg=bk0 + gfirst + gn - 1, ngroups=-(-nwp // FAN_IN), bkend=bkend)
+            pieces_of.setdefault(k, []).append((s, g))
+    ents = workgroup_entries(sim)
+    group_cnt, seg_cnt = {}, {}
     published_local, wg_published, group_published, written = set(), set(), set(), {}
     done_group, done_seg = set(), set()  # counters whose last arrival has come, not yet reset
+    at_barrier = {b: 0 for b in ents}
 
     def read(cnt, done, k):
         assert k not in done, f"counter {k} read after its last arrival"
         return cnt.get(k, 0)
 
     def steps_of(w):
-        pieces = waves[w]
-        # stage 1: publish and count every piece on its share's LDS counter
-        lasts = []
-        for info in pieces:
-            published_local.add((info["seg"], info["k"]))
-            old = wg_cnt.get(info["share"], 0)
-            wg_cnt[info["share"]] = old + 1
-            if old == len(info["share_waves"]) - 1:
-                lasts.append(info)
+        b = w // WAVES
+        for seg in pieces_of.get(w, []):
+            published_local.add((seg, w))
             yield
-        if not lasts:
-            return
-        # group counters of the shares going on to stage 2 are read before the folds
-        early = [read(group_cnt, done_group, info["kg"]) if info["nwp"] > 1 else None for info in lasts]
-        yield
+        at_barrier[b] += 1
+        while at_barrier[b] < WAVES:
+            yield
         resets = []
-        for info, c in zip(lasts, early):
-            seg = info["seg"]
-            for k in info["share_waves"]:
-                assert (seg, k) in published_local, f"share of {seg} read piece of wave {k} before it was published"
+        for seg in assign_shares(ents[b])[w % WAVES]:
+            info = info_of[(b, seg)]
+            for k in range(b * WAVES, b * WAVES + WAVES):
+                if seg in pieces_of.get(k, []):
+                    assert (seg, k) in published_local, f"share of {seg} read piece of wave {k} before it was published"
+            yield
             if info["nwp"] == 1:
                 written[seg] = written.get(seg, 0) + 1
                 continue
+            c = read(group_cnt, done_group, info["kg"])
+            yield
             if c != info["gn"] - 1:
                 wg_published.add((seg, info["rb"]))
                 old = read(group_cnt, done_group, info["kg"])
@@ -370,7 +407,7 @@ def run_merge_protocol(sim, rng):
             cnt[k] = 0
             done.discard(k)
 
-    live = {w: steps_of(w) for w in waves}
+    live = {w: steps_of(w) for b in ents for w in range(b * WAVES, b * WAVES + WAVES)}
     while live:
         w = list(live)[int(rng.integers(0, len(live)))]
         try:
@@ -380,12 +417,6 @@ def run_merge_protocol(sim, rng):
     assert written == {seg: 1 for seg in sim["pieces"]}, "a cut segment was written other than once"
     assert all(v == 0 for v in group_cnt.values()) and all(v == 0 for v in seg_cnt.values())
     assert not done_group and not done_seg
-    # every share's LDS counter saw exactly the share's pieces (no reset: LDS lives one launch)
-    shares = {}
-    for ws in waves.values():
-        for info in ws:
-            shares[info["share"]] = len(info["share_waves"])
-    assert wg_cnt == shares
 
 
 @pytest.mark.parametrize("trial", range(30))
@@ -418,3 +449,29 @@ def test_merge_protocol_two_levels(trial):
     assert -(-(pre[1] - pre[0]) // (WAVES * C)) > FAN_IN  # the long segment spans more than one group
     for rep in range(3):
         run_merge_protocol(sim, np.random.default_rng(rep + 10 * trial))
+
+
+def div_small(a, d):
+    """The kernel's a / d for quotients below 2^22: the float32 product of a
+    and the rounded reciprocal, truncated, then one correction step."""
+    rd = np.float32(1.0) / np.float32(d)
+    q = int(np.float32(np.float32(a) * rd))
+    r = a - q * d
+    return q + (1 if r >= d else 0) - (1 if r < 0 else 0)
+
+
+def test_div_small_exact():
+    """Exact for every divisor and dividend the merge uses: slice sizes C and
+    4C up to the largest streams (4096 sequences of 65,536 tokens, 16 KV heads
+    is 2^27 units), quotients up to the number of waves; edges at exact
+    multiples, one below and one above them included."""
+    rng = np.random.default_rng(11)
+    cases = []
+    for d in list(range(1, 300)) + [int(x) for x in rng.integers(1, 1 << 27, 3000)]:
+        qmax = min((1 << 27) // d + 1, (1 << 22) - 1)
+        for q in [0, 1, 2, qmax - 1, qmax] + [int(x) for x in rng.integers(0, qmax + 1, 8)]:
+            for a in (q * d - 1, q * d, q * d + 1, q * d + d - 1):
+                if 0 <= a < (1 << 31) and a // d < (1 << 22):
+                    cases.append((a, d))
+    for a, d in cases:
+        assert div_small(a, d) == a // d, (a, d)
