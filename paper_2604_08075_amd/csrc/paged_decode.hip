@@ -867,47 +867,36 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   // kWaves + 1 slice boundaries.  Share i goes to wave min(pos, kWaves - 1),
   // pos = 0 for the first share, 1 for the last, i + 1 for the others: the
   // only shares that can cross the workgroup's edges and go on to stage 2,
-  // the first and the last, run on different waves.
-  int es[2 * kWaves], eg[2 * kWaves];
-#pragma unroll
-  for (int e = 0; e < 2 * kWaves; ++e) {
-    es[e] = __builtin_amdgcn_readfirstlane(wg_seg[e][0]);
-    eg[e] = __builtin_amdgcn_readfirstlane(wg_seg[e][1]);
-  }
-  int nsh = 0;
+  // the first and the last, run on different waves.  Lane e looks at entry
+  // e: it starts a share if it is valid and differs from the closest valid
+  // entry before it.
+  int ms0 = 0, mg0 = 0, ms1 = 0, mg1 = 0;  // this wave's shares, in order
+  int mine = 0;
   {
-    int ps = -1, pg = 0;
-#pragma unroll
-    for (int e = 0; e < 2 * kWaves; ++e)
-      if (es[e] >= 0) {
-        if (es[e] != ps || eg[e] != pg) ++nsh;
-        ps = es[e];
-        pg = eg[e];
-      }
-  }
-  int mine = 0, ms0 = 0, mg0 = 0, ms1 = 0, mg1 = 0;  // this wave's shares, in order
-  {
-    int ps = -1, pg = 0, i = -1;
-#pragma unroll
-    for (int e = 0; e < 2 * kWaves; ++e)
-      if (es[e] >= 0) {
-        if (es[e] != ps || eg[e] != pg) {
-          ++i;
-          const int pos = i == 0 ? 0 : (i == nsh - 1 ? 1 : i + 1);
-          if (min(pos, kWaves - 1) == w) {
-            if (mine == 0) {
-              ms0 = es[e];
-              mg0 = eg[e];
-            } else {
-              ms1 = es[e];
-              mg1 = eg[e];
-            }
-            ++mine;
-          }
-        }
-        ps = es[e];
-        pg = eg[e];
-      }
+    int es = -1, eg = 0;
+    if (lane < 2 * kWaves) {
+      es = wg_seg[lane][0];
+      eg = wg_seg[lane][1];
+    }
+    const unsigned long long below = (1ull << lane) - 1;
+    const unsigned long long valid = __ballot(es >= 0);
+    const unsigned long long vb = valid & below;
+    const int prev = vb ? 63 - __clzll(vb) : lane;
+    const int ps = __shfl(es, prev), pg = __shfl(eg, prev);
+    const bool start = es >= 0 && (vb == 0 || ps != es || pg != eg);
+    const unsigned long long starts = __ballot(start);
+    const int nsh = __popcll(starts);
+    const int i = __popcll(starts & below);
+    const int pos = i == 0 ? 0 : (i == nsh - 1 ? 1 : i + 1);
+    const unsigned long long my = __ballot(start && min(pos, kWaves - 1) == w);
+    mine = __popcll(my);
+    const int l0 = my ? __ffsll(my) - 1 : 0;
+    const unsigned long long my1 = my & (my - 1);
+    const int l1 = my1 ? __ffsll(my1) - 1 : 0;
+    ms0 = __builtin_amdgcn_readlane(es, l0);
+    mg0 = __builtin_amdgcn_readlane(eg, l0);
+    ms1 = __builtin_amdgcn_readlane(es, l1);
+    mg1 = __builtin_amdgcn_readlane(eg, l1);
   }
   if (mine == 0) return;
 
