@@ -300,6 +300,12 @@ int32_t paged_decode_partition_tokens(const dp_decode_shape* shape);
  * out = sum_p w_p o_p / sum_p w_p: first inside each workgroup (through its
  * LDS), then, for pairs whose slices span several workgroups, the
  * workgroups' partials through the workspace, by the last to finish.
+ * The workspace also keeps, for each wave, the cache tiles its first unit
+ * read; the next call starts loading those tiles before it has found its
+ * own, and loads again where they differ.  A call with the context lengths
+ * and block tables of the previous call on the workspace (every layer of a
+ * decode step after the first) starts its reads earlier; results never
+ * depend on what the workspace holds.
  * Results are deterministic: the same inputs and shape give the same bits. */
 int paged_decode_attention(const void* q, const void* k_blocks, const void* v_blocks,
                            const int32_t* block_tables, const int32_t* context_lens,

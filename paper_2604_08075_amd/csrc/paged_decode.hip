@@ -89,6 +89,7 @@ struct DecodeArgs {
   int32_t* arrivals;            // [2, waves]: group and segment arrival counters; zero between calls
   float* rec_ml;                // [3 * waves, G, 2]    (max in log2 units, sum)
   float* rec_o;                 // [3 * waves, G, 128]  partial outputs (normalised, V-scaled)
+  int32_t* tile_cache;          // [waves, 4]: tiles of each wave's first unit in the previous call (a hint)
   float qk_scale_log2;          // scale * log2(e)
   int32_t batch, hq, hkv, group;
   int32_t max_blocks_per_seq, max_ctx;
@@ -394,6 +395,14 @@ struct Walker {
   int s, g, j, nus;
 };
 
+// A workgroup barrier that waits for LDS accesses only, not for loads or
+// stores to memory still in flight.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // a / d for a >= 0, d >= 1 and a quotient below 2^22 (a wave or workgroup
 // index): the float estimate is then off by at most one, and one step
 // corrects it.  rd = 1 / d, rounded.
@@ -425,6 +434,49 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   float* kscl = (float*)(dyn + 2 * B + 1);
   float* vscl = kscl + Hkv;
 
+  // ---- per-lane operand offsets inside a tile ----
+  int kofs[8], vofs[8];
+  int kblk, vblk;  // which block of the unit this lane's K / V fragments come from
+  if constexpr (FP8) {
+    // K: MFMA m (0..3), row li = token 4m + (li & 3) of block li >> 2; fragment j = dims 64j + 16lj .. +16
+    for (int m = 0; m < 4; ++m)
+      for (int jj = 0; jj < 2; ++jj) kofs[2 * m + jj] = (4 * m + (li & 3)) * 128 + 64 * jj + 16 * lj;
+    kblk = li >> 2;
+    // V: dim 16nn + li, all 16 tokens of block lj
+    for (int nn = 0; nn < 8; ++nn) vofs[nn] = (16 * nn + li) * 16;
+    vblk = lj;
+  } else {
+    // K: MFMA m (0..1), row li = token 8((li >> 2) & 1) + 4m + (li & 3) of block li >> 3; chunk c = dims 32c + 8lj
+    for (int m = 0; m < 2; ++m)
+      for (int c = 0; c < 4; ++c) kofs[4 * m + c] = (8 * ((li >> 2) & 1) + 4 * m + (li & 3)) * 256 + 64 * c + 16 * lj;
+    kblk = li >> 3;
+    // V: dim 16nn + li, tokens 8(lj & 1) .. +8 of block lj >> 1
+    for (int nn = 0; nn < 8; ++nn) vofs[nn] = (16 * nn + li) * 32 + 16 * (lj & 1);
+    vblk = lj >> 1;
+  }
+  auto issue_at = [&](UnitRegs& R, int kt, int vt) __attribute__((always_inline)) {
+    const char* kb = a.k + (size_t)kt * TILE;
+    const char* vb = a.v + (size_t)vt * TILE;
+#pragma unroll
+    for (int x = 0; x < 8; ++x) R.k[x] = __builtin_nontemporal_load((const i32x4*)(kb + kofs[x]));
+#pragma unroll
+    for (int x = 0; x < 8; ++x) R.v[x] = __builtin_nontemporal_load((const i32x4*)(vb + vofs[x]));
+  };
+
+  // ---- 0. the first unit's loads, from the tiles of the previous call ----
+  // Every layer of a decode step but the first repeats the previous call's
+  // context lengths and block tables, and with them each wave's first unit.
+  // A wave keeps that unit's tile indices in the workspace and issues the
+  // unit's loads from them right away, while the prologue finds the true
+  // tiles; if they differ, it loads the unit again.  The kept indices are
+  // clamped into the pool, so whatever the workspace holds only decides
+  // whether the early loads are of use.
+  const int gw = blockIdx.x * kWaves + w;
+  const int tmax = (a.num_blocks_m1 + 1) * Hkv - 1;
+  const int ck = min(max(a.tile_cache[(size_t)gw * 4 + kblk], 0), tmax);
+  const int cv = min(max(a.tile_cache[(size_t)gw * 4 + vblk], 0), tmax);
+  UnitRegs RA;
+
   // ---- 1. prefix of units over sequences (every workgroup computes it) ----
   {
     const int T = kWaves * 64, tid = threadIdx.x;
@@ -444,13 +496,14 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
         local += units_of<FP8>(c);
       }
     }
+    issue_at(RA, ck, cv);
     int incl = local;
     for (int off = 1; off < 64; off <<= 1) {
       const int v = __shfl_up(incl, off);
       if (lane >= off) incl += v;
     }
     if (lane == 63) wave_sums[w] = incl;
-    __syncthreads();
+    lds_barrier();  // (LDS only: the first unit's loads stay in flight)
     int run = incl - local;
     for (int k = 0; k < w; ++k) run += wave_sums[k];
     for (int k = 0; k < per; ++k) {
@@ -461,14 +514,13 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       }
     }
     if (tid == T - 1) pre[B] = run;
-    __syncthreads();
+    lds_barrier();
   }
   const int U = Hkv * pre[B];
   const int TW = gridDim.x * kWaves;
   int C = (U + TW - 1) / TW;
   if (C < a.min_chunk) C = a.min_chunk;
   const float rC = 1.0f / (float)C, rCW = 1.0f / (float)(kWaves * C);  // for the merge's slice arithmetic
-  const int gw = blockIdx.x * kWaves + w;
 
   // rows of empty sequences are zero
   for (int s = gw; s < B; s += TW) {
@@ -522,27 +574,10 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
         tiles[i * UB + b] = id * Hkv + g;
       }
     }
+    // the early loads were of the first unit's true tiles, or it is loaded again
+    if (__ballot(tiles[kblk] != ck || tiles[vblk] != cv)) issue_at(RA, tiles[kblk], tiles[vblk]);
+    if (lane < UB) a.tile_cache[(size_t)gw * 4 + lane] = tiles[lane];
 
-    // ---- 3. per-lane operand offsets inside a tile ----
-    int kofs[8], vofs[8];
-    int kblk, vblk;  // which block of the unit this lane's K / V fragments come from
-    if constexpr (FP8) {
-      // K: MFMA m (0..3), row li = token 4m + (li & 3) of block li >> 2; fragment j = dims 64j + 16lj .. +16
-      for (int m = 0; m < 4; ++m)
-        for (int jj = 0; jj < 2; ++jj) kofs[2 * m + jj] = (4 * m + (li & 3)) * 128 + 64 * jj + 16 * lj;
-      kblk = li >> 2;
-      // V: dim 16nn + li, all 16 tokens of block lj
-      for (int nn = 0; nn < 8; ++nn) vofs[nn] = (16 * nn + li) * 16;
-      vblk = lj;
-    } else {
-      // K: MFMA m (0..1), row li = token 8((li >> 2) & 1) + 4m + (li & 3) of block li >> 3; chunk c = dims 32c + 8lj
-      for (int m = 0; m < 2; ++m)
-        for (int c = 0; c < 4; ++c) kofs[4 * m + c] = (8 * ((li >> 2) & 1) + 4 * m + (li & 3)) * 256 + 64 * c + 16 * lj;
-      kblk = li >> 3;
-      // V: dim 16nn + li, tokens 8(lj & 1) .. +8 of block lj >> 1
-      for (int nn = 0; nn < 8; ++nn) vofs[nn] = (16 * nn + li) * 32 + 16 * (lj & 1);
-      vblk = lj >> 1;
-    }
     // query fragment c of head li: the dims its K fragment holds.  Columns past
     // the GQA group repeat a real head; they only ever affect their own
     // (unwritten) output columns.
@@ -579,12 +614,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       for (int c = 0; c < 4; ++c) qr[c] = *(const i32x4*)(qrow + qoff[c]);
     };
     auto issue = [&](UnitRegs& R, int ui) __attribute__((always_inline)) {
-      const char* kb = a.k + (size_t)tiles[ui * UB + kblk] * TILE;
-      const char* vb = a.v + (size_t)tiles[ui * UB + vblk] * TILE;
-#pragma unroll
-      for (int x = 0; x < 8; ++x) R.k[x] = __builtin_nontemporal_load((const i32x4*)(kb + kofs[x]));
-#pragma unroll
-      for (int x = 0; x < 8; ++x) R.v[x] = __builtin_nontemporal_load((const i32x4*)(vb + vofs[x]));
+      issue_at(R, tiles[ui * UB + kblk], tiles[ui * UB + vblk]);
     };
 
     // ---- the records of this wave's split pieces, in LDS ----
@@ -761,10 +791,9 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
     advance(w1);
     w2 = w1;
     advance(w2);
-    UnitRegs RA, RB;
+    UnitRegs RB;  // (RA holds the first unit)
     load_q(qE, cs.s, cs.g);
     load_q(qO, w1.s, w1.g);
-    issue(RA, 0);
     auto step = [&](UnitRegs& cur, UnitRegs& nxt, i32x4 (&qs)[4], int ui) __attribute__((always_inline)) {
       issue(nxt, ui + 1);
       // keep the compiler's scheduler from hoisting the computation of unit u
@@ -859,9 +888,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
   }
   // Every record and entry of the workgroup is in LDS after this barrier (it
   // waits for LDS accesses only, not for the rows' stores to memory).
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+  lds_barrier();
   // The shares are the runs of equal segments among the entries (wave, x),
   // in order: at most kWaves + 1, as each crosses one of the workgroup's
   // kWaves + 1 slice boundaries.  Share i goes to wave min(pos, kWaves - 1),
@@ -1092,7 +1119,7 @@ struct Plan {
   int min_chunk;    // minimum units per slice
   int grid;         // workgroups
   size_t dyn_lds;   // dynamic LDS bytes
-  size_t arrivals_off, rec_ml_off, rec_o_off, ws_bytes;
+  size_t arrivals_off, rec_ml_off, rec_o_off, tile_cache_off, ws_bytes;
   int clear_words;  // arrival counters to zero before the launch (0 on the usual path)
 };
 
@@ -1173,7 +1200,9 @@ int validate(const dp_decode_shape* sh, Plan* plan) {
   plan->rec_ml_off = align256(2 * counter_waves * sizeof(int32_t));
   // records: two workgroup pieces and one group record per workgroup
   plan->rec_o_off = plan->rec_ml_off + align256(3 * (size_t)grid * G * 2 * sizeof(float));
-  plan->ws_bytes = plan->rec_o_off + align256(3 * (size_t)grid * G * kHeadDim * sizeof(float));
+  plan->tile_cache_off = plan->rec_o_off + align256(3 * (size_t)grid * G * kHeadDim * sizeof(float));
+  // each wave's first-unit tiles, kept for the next call (any content is safe)
+  plan->ws_bytes = plan->tile_cache_off + align256(waves * 4 * sizeof(int32_t));
   return DP_OK;
 }
 
@@ -1232,6 +1261,7 @@ extern "C" int paged_decode_attention(const void* q, const void* k_blocks, const
   a.arrivals = (int32_t*)((char*)workspace + plan.arrivals_off);
   a.rec_ml = (float*)((char*)workspace + plan.rec_ml_off);
   a.rec_o = (float*)((char*)workspace + plan.rec_o_off);
+  a.tile_cache = (int32_t*)((char*)workspace + plan.tile_cache_off);
   a.qk_scale_log2 = scale * kLog2e;
   a.batch = shape->batch;
   a.hq = shape->n_q_heads;

@@ -157,21 +157,49 @@ def test_empty_context_gives_zero_rows(gpu_lib):
         assert max_err(got, ref, [1, 3]) <= TOL["bf16"]
 
 
-def test_block_permutation_is_bit_exact(gpu_lib):
-    note("block permutation")
-    w = workloads.make_workload(6, 64, 8, [5, 300, 1024, 17, 2000, 64], c_max=2048, seed=6, num_blocks=600)
-    base = gpu_out(gpu_lib, w)
-    rng = np.random.default_rng(0)
-    pi = rng.permutation(w.num_blocks)
-    w2 = workloads.make_workload(6, 64, 8, [5, 300, 1024, 17, 2000, 64], c_max=2048, seed=6, num_blocks=600)
-    # move each physical block b to pi[b] and fix the table up
-    for st in (w2.k_store, w2.v_store):
+def renumbered(ctx, seed, perm_seed):
+    """The workload of make_workload(6, 64, 8, ctx, seed) with every physical
+    block b moved to pi[b] and the block table fixed up."""
+    w = workloads.make_workload(6, 64, 8, ctx, c_max=2048, seed=seed, num_blocks=600)
+    pi = np.random.default_rng(perm_seed).permutation(w.num_blocks)
+    for st in (w.k_store, w.v_store):
         st.used_ids = pi[st.used_ids]
         st.slot = np.full(st.num_blocks, -1, dtype=np.int64)
         st.slot[st.used_ids] = np.arange(len(st.used_ids))
-    w2.block_tables = np.where(w.block_tables >= 0, pi[np.maximum(w.block_tables, 0)], -1).astype(np.int32)
-    moved = gpu_out(gpu_lib, w2)
+    w.block_tables = np.where(w.block_tables >= 0, pi[np.maximum(w.block_tables, 0)], -1).astype(np.int32)
+    return w
+
+
+def test_block_permutation_is_bit_exact(gpu_lib):
+    note("block permutation")
+    ctx = [5, 300, 1024, 17, 2000, 64]
+    w = workloads.make_workload(6, 64, 8, ctx, c_max=2048, seed=6, num_blocks=600)
+    base = gpu_out(gpu_lib, w)
+    moved = gpu_out(gpu_lib, renumbered(ctx, 6, 0))
     assert np.array_equal(moved, base)
+
+
+def test_first_unit_hint_follows_changed_inputs(gpu_lib):
+    """A wave issues its first unit's loads from the tiles the previous call on the
+    same workspace used, and loads the unit again when the true tiles differ.
+    One workspace, calls alternating between the same contexts with the blocks
+    renumbered and different context lengths (other slices): every call equals
+    its result on a fresh workspace bit for bit."""
+    note("first-unit hint: alternating inputs on one workspace")
+    ctx = [5, 300, 1024, 17, 2000, 64]
+    ws = [workloads.make_workload(6, 64, 8, ctx, c_max=2048, seed=6, num_blocks=600), renumbered(ctx, 6, 0),
+          workloads.make_workload(6, 64, 8, [700, 1, 1500, 2048, 90, 333], c_max=2048, seed=16, num_blocks=600)]
+    assert len({(w.max_blocks_per_seq, w.num_blocks) for w in ws}) == 1
+    devs = [workloads.to_device(w) for w in ws]
+
+    def decoder():  # one shape for every call: C_max 2048
+        return gpu_lib.PagedDecoder(6, 64, 8, ws[0].max_blocks_per_seq, 2048, ws[0].num_blocks)
+
+    fresh = [gpu_out(gpu_lib, w, d, dec=decoder()) for w, d in zip(ws, devs)]
+    dec = decoder()
+    for i in (0, 0, 1, 1, 0, 2, 2, 1, 0):
+        got = gpu_out(gpu_lib, ws[i], devs[i], dec=dec)
+        assert np.array_equal(got, fresh[i]), f"call on input {i} differs from its fresh-workspace result"
 
 
 def test_unused_blocks_never_read(gpu_lib):
