@@ -20,10 +20,18 @@
 // segment boundaries without draining its load pipeline.  A segment that
 // lies wholly inside one slice is finished in registers and written to
 // `out`; a segment cut by slice boundaries leaves one softmax partial per
-// piece (a wave has at most two such pieces: its first and its last).  At the
-// end of its slice a wave signals its pieces on per-segment arrival counters;
-// the wave that brings a segment's last piece merges the partials with
-// log-sum-exp weights, reading them in a fixed order (deterministic).
+// piece (a wave has at most two such pieces: its first and its last), kept
+// in the wave's LDS.  After a workgroup barrier each share of a cut segment
+// held by the workgroup is merged by one of its waves, with log-sum-exp
+// weights; a share that crosses the workgroup's edges then goes through
+// device-wide arrival counters, and the workgroup that brings a group's last
+// piece merges the group.  Every fold reads its partials in a fixed order
+// (deterministic).
+//
+// A wave's first unit is issued at launch from the tiles it used in the
+// previous call on the same workspace (every layer of a decode step but the
+// first has the same context lengths and block tables), and loaded again if
+// the true tiles, found by the prologue, differ.
 //
 // Per wave, the hot loop keeps one unit in flight while it computes the
 // previous one, with every byte going straight to registers in the layout
@@ -72,10 +80,10 @@ constexpr int kBlock = 16;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kWaves = 4;              // waves per workgroup
 constexpr int kMaxUnitsPerWave = 256;  // the host sizes the grid so that no slice is longer
-// Finished output rows and partial records are staged in LDS and written out
-// after the loop (global stores share the in-order memory counter with the
-// KV loads; a store issued inside the loop would make the next wait cover it).
-constexpr int kRecBytes = 8192 + 512;  // a staged record: eight 1 KiB chunks of o, then (m, l) per lane
+// A piece's partial stays in its wave's LDS until the merge (no global store
+// inside the loop, where stores would share the in-order memory counter with
+// the KV loads).
+constexpr int kRecBytes = 8192 + 512;  // a record in LDS: eight 1 KiB chunks of o, then (m, l) per lane
 
 struct DecodeArgs {
   const uint16_t* q;            // [B, Hq, 128] bf16
