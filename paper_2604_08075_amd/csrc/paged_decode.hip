@@ -403,6 +403,20 @@ struct Walker {
   int s, g, j, nus;
 };
 
+// Inclusive prefix sum over the 64 lanes of a wave, in the vector ALU (no
+// LDS round trips): data-parallel-primitive moves shift each 16-lane row
+// right by 1, 2, 4 and 8 lanes (a lane with no source adds 0), then lane 15
+// of rows 0 and 2 is added into rows 1 and 3, and lane 31 into rows 2 and 3.
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15 into rows 1, 3
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31 into rows 2, 3
+  return x;
+}
+
 // A workgroup barrier that waits for LDS accesses only, not for loads or
 // stores to memory still in flight.
 __device__ __forceinline__ void lds_barrier() {
@@ -505,11 +519,7 @@ __global__ __launch_bounds__(kWaves * 64) void paged_decode_kernel(DecodeArgs a)
       }
     }
     issue_at(RA, ck, cv);
-    int incl = local;
-    for (int off = 1; off < 64; off <<= 1) {
-      const int v = __shfl_up(incl, off);
-      if (lane >= off) incl += v;
-    }
+    const int incl = wave_incl_scan(local);
     if (lane == 63) wave_sums[w] = incl;
     lds_barrier();  // (LDS only: the first unit's loads stay in flight)
     int run = incl - local;
