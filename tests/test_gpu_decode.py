@@ -108,6 +108,39 @@ def test_random_shapes_ragged(gpu_lib, kv, G, P):
     assert err <= TOL[kv]
 
 
+def test_random_batches_every_row(gpu_lib):
+    """Sixty seeded random decode shapes (cache format, GQA group 1-16, 1-8 KV
+    heads, 1-130 sequences with empty ones among them, C_max 64-5000, minimum
+    slice and workgroups per compute unit), every row against the oracle.  Each
+    shape is called twice on one workspace: the second call starts its first
+    unit from the tiles the first call kept, and must equal it bit for bit."""
+    rng = np.random.default_rng(2604)
+    for case in range(60):
+        kv = ["bf16", "fp8_e4m3"][int(rng.integers(0, 2))]
+        G = int(rng.choice([1, 2, 4, 8, 16]))
+        Hkv = int(rng.choice([1, 2, 4, 8]))
+        B = int(rng.choice([1, 2, 3, 7, 16, 33, 64, 130]))
+        cmax = int(rng.choice([64, 700, 2048, 5000]))
+        ctx = rng.integers(0, cmax + 1, B)
+        if rng.random() < 0.3:
+            ctx[rng.random(B) < 0.5] = 0
+        if ctx.max() == 0:
+            ctx[0] = 1
+        P = int(rng.choice([0, 0, 64, 128, 512]))
+        wgs = int(rng.choice([0, 0, 1, 2]))
+        seed = int(rng.integers(0, 1 << 30))
+        note(f"case {case}: kv={kv} G={G} Hkv={Hkv} B={B} C_max={cmax} P={P} wgs={wgs} seed={seed}")
+        w = workloads.make_workload(B, G * Hkv, Hkv, list(ctx), c_max=cmax, kv_format=kv, seed=seed)
+        d = workloads.to_device(w)
+        dec = gpu_lib.PagedDecoder(w.batch, w.n_q_heads, w.n_kv_heads, w.max_blocks_per_seq, w.max_context_len,
+                                   w.num_blocks, kv_fp8=kv == "fp8_e4m3", out_fp32=True, partition_tokens=P,
+                                   workgroups_per_cu=wgs)
+        first = gpu_out(gpu_lib, w, d, dec=dec)
+        assert np.array_equal(gpu_out(gpu_lib, w, d, dec=dec), first), "the second call differs from the first"
+        err = max_err(first, oracle_out(w), list(range(B)))
+        assert np.isfinite(first).all() and err <= TOL[kv], f"case {case}: max abs err {err:.3e}"
+
+
 def test_partition_invariance(gpu_lib):
     """Different split-K partitionings agree to the bound the arithmetic gives.
 
